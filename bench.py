@@ -1,0 +1,244 @@
+"""Benchmark of the LayUp layer-wise step on one MI355X.
+
+A step is one pass of the whole path on one batch of synthetic data: forward
+pass and loss, then for every unit from the output back to the input its
+backward GEMMs and glue kernels on the compute stream and, overlapped on the
+update stream, its fused AdamW update + gossip mix with the peer replica
+(LayUp Algorithm 1 with the layer-wise updates of section 3.2).  Workload:
+GPT-2-small-shaped decoder, 12 blocks x 768, 12 heads, MLP 3072, T 1024,
+batch 8, vocab 50257 (tokens uniform, weights N(0, 0.02), peer = weights +
+N(0, 1e-3)), AdamW (0.9, 0.95), wd 0.1 on matrices, alpha 0.5.
+
+Prints ONE JSON line.  ``value`` is ms per layer-wise step (lower is better);
+the per-kernel figures (update+mix HBM GB/s, backward-GEMM TFLOP/s) are
+measured with HIP events on the stream the kernels run on.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, TFLOP/s
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--kernel-reps", type=int, default=20)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
+    return ap.parse_args()
+
+
+def backward_gemm_shapes(cfg):
+    """(name, M, N, K, a_kmajor, b_kmajor) of one block's dX/dW GEMMs and the
+    tied head's, at the workload's shape (N_tok = batch * seq)."""
+    n, d, f, vp = cfg.batch * cfg.seq, cfg.d_model, cfg.d_ff, (cfg.vocab + 63) // 64 * 64
+    out = []
+    for name, o, i in (("qkv", 3 * d, d), ("proj", d, d), ("fc", f, d), ("mproj", d, f)):
+        out.append((name + ".dX", n, i, o, True, False))
+        out.append((name + ".dW", o, i, n, False, False))
+    head = [("head.dX", n, d, vp, True, False), ("head.dW", vp, d, n, False, False)]
+    return out, head
+
+
+def time_gemms(torch, LU, shapes, reps, stream):
+    """Average duration of each GEMM launch with HIP events on its stream."""
+    res = []
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    for name, M, N, K, ak, bk in shapes:
+        A = torch.randn((M, K) if ak else (K, M), device="cuda").to(torch.bfloat16)
+        B = torch.randn((N, K) if bk else (K, N), device="cuda").to(torch.bfloat16)
+        C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        d = LU.gemm_desc(A, B, C, M, N, K, K if ak else M, K if bk else N, N, ak, bk, True,
+                         workspace=ws, workspace_bytes=64 << 20)
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                LU.layup_gemm_bf16(d, stream)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                LU.layup_gemm_bf16(d, stream)
+            e1.record(stream)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res.append(dict(name=name, M=M, N=N, K=K, ms=ms, tflops=2.0 * M * N * K / (ms * 1e-3) / 1e12))
+    return res
+
+
+def time_update_mix(torch, LU, m, unit, hp, alpha, reps, stream, flush):
+    """Average duration of one unit's update+mix launch (AdamW + bf16 copy)
+    with HIP events on the update stream; the 512 MB flush buffer is
+    rewritten between launches so the unit's 241 MB are not served from the
+    256 MB MALL."""
+    t = [x for x in m.infos if x["unit"] == unit]
+    numel = sum(x["numel"] for x in t)
+    descs = []
+    for x in t:
+        o = x["offset"]
+        descs.append(LU.layup_tensor(param=m.params.data_ptr() + 4 * o, grad=m.grads.data_ptr() + 4 * o,
+                                     state0=m.m.data_ptr() + 4 * o, state1=m.v.data_ptr() + 4 * o,
+                                     peer=m.peers.data_ptr() + 4 * o,
+                                     param_bf16=m.params_bf16.data_ptr() + 2 * o,
+                                     numel=x["numel"], decay=x["decay"]))
+    ms_tot = 0.0
+    hp.step = 1
+    with torch.cuda.stream(stream):
+        for r in range(reps + 2):
+            flush.add_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            LU.layup_layer_update_mix(None, descs, hp, alpha, stream=stream)
+            e1.record(stream)
+            e1.synchronize()
+            if r >= 2:
+                ms_tot += e0.elapsed_time(e1)
+    ms = ms_tot / reps
+    nbytes = 34 * numel   # AdamW 32 B/param + 2 B bf16 copy
+    return dict(unit=unit, numel=numel, ms=ms, bytes=nbytes, gbs=nbytes / (ms * 1e-3) / 1e9)
+
+
+def cpu_baseline(cfg_full):
+    """The oracle on the host cores: one whole layer-wise step of a stack with
+    the full width, sequence length and vocabulary but 1 block and 2 of the 8
+    sequences, scaled to the full step by the ratio of the two steps' GEMM
+    FLOPs (the oracle's time is dominated by its float64 matrix products)."""
+    import threadpoolctl
+    import oracle as O
+    from paper_2410_05985_amd import synthetic as S
+    cfg1 = S.GPTConfig(n_layer=1, d_model=cfg_full.d_model, n_head=cfg_full.n_head,
+                       d_ff=cfg_full.d_ff, seq=cfg_full.seq, batch=2,
+                       vocab=cfg_full.vocab)
+    params = {k: v.astype(np.float64) for k, v in S.gpt_params(cfg1).items()}
+    peer = {k: v.astype(np.float64) for k, v in S.gpt_peer(cfg1, S.gpt_params(cfg1)).items()}
+    tokens = S.gpt_tokens(cfg1)
+    m = {k: np.zeros_like(v) for k, v in params.items()}
+    v = {k: np.zeros_like(v_) for k, v_ in params.items()}
+    hp = dict(optim="adamw", lr=cfg1.lr, weight_decay=cfg1.weight_decay, beta1=cfg1.beta1,
+              beta2=cfg1.beta2, eps=cfg1.eps)
+    threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
+    t0 = time.perf_counter()
+    O.gpt_step(params, m, v, peer, tokens, cfg1.n_head, hp, cfg1.alpha)
+    dt = time.perf_counter() - t0
+
+    def flops(c):
+        n, d, f, V = c.batch * c.seq, c.d_model, c.d_ff, c.vocab
+        blk = 2 * n * (3 * d * d + d * d + 2 * d * f) * 3 + 4 * c.batch * c.seq * c.seq * d * 3
+        return c.n_layer * blk + 2 * n * d * V * 3
+    scale = flops(cfg_full) / flops(cfg1)
+    return dict(value=dt * scale * 1e3, unit="ms/step", cores=int(threads), kind="oracle",
+                sample=f"one oracle step of a 1-block, batch-2 stack at full width/seq/vocab "
+                       f"({dt:.1f} s), scaled by GEMM FLOPs x{scale:.2f} to 12 blocks x batch 8")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU: the layer-wise step of one worker; "
+                                   "multi-GPU runs are not part of it", "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    from paper_2410_05985_amd import layup as LU
+    from paper_2410_05985_amd import synthetic as S
+
+    cfg = S.GPT2_SMALL
+    params = S.gpt_params(cfg)
+    tokens = S.gpt_tokens(cfg)
+    peer = S.gpt_peer(cfg, params)
+    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch, cfg.vocab)
+    model = LU.Model(lc, "adamw", two_streams=not args.serialize)
+    model.load("params", params)
+    model.load("peers", peer)
+    del params, peer
+    td = torch.from_numpy(tokens).to("cuda")
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, 1)
+    torch.cuda.synchronize()
+    step = 0
+    for _ in range(args.warmup):
+        step += 1
+        hp.step = step
+        LU.layup_step(model.ctx, td, None, hp, cfg.alpha, 0, loss)
+    model.synchronize()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step += 1
+        hp.step = step
+        LU.layup_step(model.ctx, td, None, hp, cfg.alpha, 0, loss)
+    model.synchronize()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    loss_v = float(loss.item())
+    print(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, loss {loss_v:.4f}", file=sys.stderr,
+          flush=True)
+
+    # per-kernel timing with HIP events on the stream the kernels run on
+    ks = torch.cuda.Stream()
+    blk, head = backward_gemm_shapes(cfg)
+    g = time_gemms(torch, LU, blk + head, args.kernel_reps, ks)
+    blk_ms = sum(x["ms"] for x in g[:len(blk)])
+    blk_flops = sum(2.0 * x["M"] * x["N"] * x["K"] for x in g[:len(blk)])
+    gemm_tflops = blk_flops / (blk_ms * 1e-3) / 1e12
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    um = time_update_mix(torch, LU, model, 1, hp, cfg.alpha, args.kernel_reps, ks, flush)
+    for x in g:
+        print(f"[bench] gemm {x['name']:9s} {x['M']}x{x['N']}x{x['K']}: {x['ms']*1e3:8.1f} us "
+              f"{x['tflops']:7.1f} TFLOP/s", file=sys.stderr, flush=True)
+    print(f"[bench] update+mix block unit: {um['ms']*1e3:.1f} us {um['gbs']:.0f} GB/s",
+          file=sys.stderr, flush=True)
+
+    # dominant kernel of the step: the backward GEMMs of a block (MFMA bound)
+    roofline = dict(bound="mfma", achieved=round(gemm_tflops, 2), peak=PEAK_BF16_TFLOPS,
+                    unit="TFLOP/s", frac=round(gemm_tflops / PEAK_BF16_TFLOPS, 4), traffic=None,
+                    kernel="gemm_bf16_kernel (one block's 8 backward dX/dW GEMMs)",
+                    algorithmic_flops_per_block=blk_flops)
+    out = {
+        "metric": "update+mix HBM GB/s; backward GEMM TFLOPS; ms per layer-wise step (GPT-2-small)",
+        "value": round(ms_step, 4),
+        "unit": "ms/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 GEMM operands / f32 accumulate, f32 master + AdamW + mix",
+        "data": "synthetic",
+        "config": {"workload": "gpt2-small layer-wise step: 12x768, 12 heads, MLP 3072, seq 1024, "
+                               "batch 8, vocab 50257, AdamW, alpha 0.5",
+                   "global_batch": cfg.batch, "seq_len": cfg.seq, "parallelism": "single worker",
+                   "streams": 1 if args.serialize else 2},
+        "tokens_per_s": round(cfg.batch * cfg.seq / (ms_step * 1e-3), 1),
+        "update_mix_GBps": round(um["gbs"], 1),
+        "update_mix_frac_hbm": round(um["gbs"] / PEAK_HBM_GBS, 4),
+        "backward_gemm_TFLOPs": round(gemm_tflops, 2),
+        "head_gemm_TFLOPs": [round(x["tflops"], 1) for x in g[len(blk):]],
+        "loss": round(loss_v, 5),
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(cfg)
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

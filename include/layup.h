@@ -1,0 +1,276 @@
+/*
+ * layup.h -- C ABI of the LayUp layer-wise backward -> update -> gossip-mix
+ * step on one AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes (LayUp, Algorithm 1, one worker):
+ *   forward pass, loss;  then for every layer ("unit") from the output back to
+ *   the input: that layer's backward pass (dX and dW GEMMs), the local
+ *   optimizer update of that layer as soon as its gradient exists (section
+ *   3.2, layer-wise updates; Algorithm 1 "Local Update"), and the weighted
+ *   average of the updated layer with a peer replica's copy of the same layer
+ *   (Algorithm 1 "Peer Update", push-sum weights of section 3.1):
+ *       p <- (1 - alpha) * p + alpha * q.
+ *   The peer copy q is a device buffer supplied by the caller (it stands in for
+ *   the gossip message of the multi-device system).  The update of layer u runs
+ *   on a second HIP stream and overlaps the backward of layer u-1 (the paper's
+ *   overlap of communication/update with computation, figure 1).
+ *
+ * Conventions
+ *   - Every pointer named "device" is HIP device memory owned by the caller.
+ *     The library never allocates or frees device memory; it owns only the
+ *     context, HIP events and host-side tables.
+ *   - Streams are hipStream_t values passed as void*.  NULL means the
+ *     context's compute stream (or the default stream where no context is
+ *     involved).
+ *   - Calls only enqueue work; they return before the GPU finishes.  Argument
+ *     errors are detected synchronously and nothing is enqueued then.
+ *     Asynchronous device faults surface at layup_synchronize or at the next
+ *     HIP call.
+ *   - A context is not thread-safe: one host thread per context.
+ *   - bf16 buffers are uint16_t bit patterns of bfloat16 values.
+ *   - Every function returns a layup_status; the text of the last error of a
+ *     context is returned by layup_last_error (context-free calls report
+ *     through layup_global_error).  No C++ exception crosses this ABI.
+ */
+#ifndef LAYUP_H
+#define LAYUP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct layup_ctx layup_ctx;
+
+typedef enum {
+  LAYUP_OK = 0,
+  LAYUP_ERR_INVALID_ARG = 1, /* null pointer, out-of-range index or value */
+  LAYUP_ERR_SHAPE = 2,       /* dimensions inconsistent or unsupported */
+  LAYUP_ERR_ALIGN = 3,       /* pointer or leading dimension misaligned */
+  LAYUP_ERR_DTYPE = 4,       /* unsupported precision / model combination */
+  LAYUP_ERR_STATE = 5,       /* call out of order (e.g. backward before forward) */
+  LAYUP_ERR_HIP = 6          /* a HIP runtime call failed; see the error text */
+} layup_status;
+
+typedef enum { LAYUP_SGD_MOMENTUM = 0, LAYUP_ADAMW = 1 } layup_optim;
+
+/* Optimizer hyperparameters of the local update (Algorithm 1 "Local Update",
+ * realised as the optimizers of the experiments, LibTorch semantics):
+ *   SGD momentum: g' = g + wd*p (decayed tensors only); m = momentum*m + g';
+ *                 p = p - lr*m.
+ *   AdamW:        p *= 1 - lr*wd (decayed tensors only);
+ *                 m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g^2;
+ *                 p -= lr/(1-b1^t) * m / (sqrt(v)/sqrt(1-b2^t) + eps).
+ * step is t >= 1 (AdamW bias correction; unused by SGD). */
+typedef struct {
+  int32_t kind; /* layup_optim */
+  float lr, momentum, weight_decay, beta1, beta2, eps;
+  int64_t step;
+} layup_hparams;
+
+/* One tensor of a layer for the fused update+mix.  All pointers are device
+ * pointers, 16-byte aligned.  param/state0/state1/param_bf16 are updated in
+ * place; grad and peer are read only; param must alias neither.  state0 is
+ * the momentum (SGD) or first moment m (AdamW); state1 the second moment v
+ * (AdamW; ignored for SGD).  param_bf16 is an optional bfloat16 copy that is
+ * rewritten from the mixed float32 value (may be NULL).  decay selects weight
+ * decay for this tensor. */
+typedef struct {
+  float* param;
+  const float* grad;
+  float* state0;
+  float* state1;
+  const float* peer;
+  uint16_t* param_bf16;
+  int64_t numel;
+  int32_t decay;
+  int32_t reserved;
+} layup_tensor;
+
+/* ---------------------------------------------------------------- models */
+
+typedef enum {
+  LAYUP_MODEL_MLP_F32 = 0,  /* ReLU MLP, float32 everywhere, softmax CE */
+  LAYUP_MODEL_GPT_BF16 = 1  /* GPT-2 decoder: bf16 GEMM operands and
+                               activations, float32 master weights */
+} layup_model;
+
+#define LAYUP_MAX_MLP_LAYERS 8
+
+/* Model description.  MLP: n_mlp_layers linear layers with
+ * mlp_dims[0] -> mlp_dims[1] -> ... -> mlp_dims[n_mlp_layers] and ReLU between
+ * them; batch rows per step.  GPT: n_layer blocks of width d_model, n_head
+ * heads, MLP width d_ff, sequence length seq, batch sequences, logical
+ * vocabulary vocab (the output head is tied with the token embedding).
+ * n_peers is the number of resident peer replicas (>= 1). */
+typedef struct {
+  int32_t model;
+  int32_t n_mlp_layers;
+  int32_t mlp_dims[LAYUP_MAX_MLP_LAYERS + 1];
+  int32_t n_layer, d_model, n_head, d_ff, seq, vocab;
+  int32_t batch;
+  int32_t n_peers;
+} layup_config;
+
+/* Where one parameter tensor lives inside the flat parameter buffer.  All
+ * flat buffers (params, grads, state0, state1, every peer replica) share this
+ * layout.  Tensors are grouped by unit; within a unit decayed tensors come
+ * first.  Offsets are multiples of 64 elements.  rows x cols is the logical
+ * shape (cols = 1 for vectors); the token embedding is stored with
+ * padded_rows rows (vocabulary rounded up to a multiple of 64), the padding
+ * rows must be zero in params and peers and are never updated. */
+typedef struct {
+  char name[32];
+  int64_t offset;
+  int64_t numel;       /* logical elements (rows * cols) */
+  int32_t rows, cols, padded_rows;
+  int32_t unit;
+  int32_t decay;
+  int32_t reserved;
+} layup_tensor_info;
+
+layup_status layup_param_layout(const layup_config* cfg, int32_t* n_tensors, int32_t* n_units,
+                                int64_t* total_elems);
+layup_status layup_tensor_layout(const layup_config* cfg, int32_t index, layup_tensor_info* out);
+
+/* Caller-owned device buffers of a model (all in the flat layout above).
+ * peers holds n_peers replicas back to back (n_peers * total_elems floats).
+ * params_bf16 is required for GPT (the GEMMs read weights from it) and
+ * ignored for the MLP.  v is required for AdamW.  trace (nullable) receives
+ * (step, unit) int32 pairs, one per unit update, in the order the updates
+ * run; trace_counter (device int32, required with trace) counts appended
+ * pairs and is never reset by the library. */
+typedef struct {
+  float* params;
+  float* grads;
+  float* m;
+  float* v;
+  const float* peers;
+  uint16_t* params_bf16;
+  int32_t* trace;
+  int32_t* trace_counter;
+  int32_t trace_capacity; /* pairs */
+  int32_t reserved;
+} layup_buffers;
+
+/* Bytes of device workspace (activations saved by the forward, gradient
+ * scratch, split-K partials) the model needs; 256-byte alignment. */
+layup_status layup_workspace_size(const layup_config* cfg, size_t* bytes);
+
+/* Create a context.  workspace: device, >= layup_workspace_size bytes,
+ * 256-byte aligned.  compute_stream runs forward and backward;
+ * update_stream runs the per-unit update+mix (may equal compute_stream,
+ * which serialises the two).  Streams must be default priority. */
+layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_buffers* bufs,
+                        void* workspace, size_t workspace_bytes, void* compute_stream,
+                        void* update_stream);
+void layup_destroy(layup_ctx* ctx);
+const char* layup_last_error(const layup_ctx* ctx);
+const char* layup_global_error(void);
+layup_status layup_synchronize(layup_ctx* ctx);
+
+/* Rewrite params_bf16 from params for every unit (call after the caller
+ * changes params outside the library).  Enqueued on the compute stream. */
+layup_status layup_refresh_shadow(layup_ctx* ctx);
+
+/* Forward pass and loss (Algorithm 1 "Forward pass"), followed by the
+ * gradient of the mean loss with respect to the logits.
+ *   GPT: tokens device int32 [batch, seq+1]; inputs are tokens[:, :seq],
+ *        targets tokens[:, 1:].  x must be NULL.
+ *   MLP: tokens device int32 [batch] class labels; x device float32
+ *        [batch, mlp_dims[0]].
+ * loss_out: device float32 scalar (nullable).  Enqueued on the compute
+ * stream.  Valid only once the previous step's updates are done (the library
+ * orders this itself through the streams). */
+layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x, float* loss_out);
+
+/* Backward pass of one unit (Algorithm 1 "Backward pass at layer l"):
+ * writes the unit's parameter gradients into grads and the gradient with
+ * respect to the unit's input into the workspace, then records the unit's
+ * "gradient ready" event (Algorithm 1 "Notify").  Units must be called in
+ * reverse order n_units-1 ... 0 after layup_forward. */
+layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit);
+
+/* Update+mix of one unit of the model (Algorithm 1 "Local Update" and "Peer
+ * Update") on the update stream, after the unit's gradient-ready event.
+ * peer_slot selects the resident peer replica.  disagreement (device float,
+ * nullable) receives sum((p_updated - q)^2) over the unit, taken before the
+ * mix.  Appends (step, unit) to the trace. */
+layup_status layup_unit_update_mix(layup_ctx* ctx, int32_t unit, const layup_hparams* hp,
+                                   float alpha, int32_t peer_slot, float* disagreement);
+
+/* Fused update+mix of arbitrary tensors (one layer of any model), single pass,
+ * HBM bound: reads p, g, m, (v), q once and writes p, m, (v), (p_bf16) once.
+ * ctx may be NULL; stream NULL = the context's update stream (or the default
+ * stream without a context).  disagreement as above (summed over the
+ * tensors).  n_tensors >= 1. */
+layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
+                                    const layup_hparams* hp, float alpha, float* disagreement,
+                                    void* stream);
+
+/* One whole layer-wise step: forward, then for u = n_units-1 ... 0:
+ * layup_layer_backward(u) on the compute stream and
+ * layup_unit_update_mix(u) on the update stream, then the compute stream
+ * waits for the update stream (join). */
+layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x,
+                        const layup_hparams* hp, float alpha, int32_t peer_slot, float* loss_out,
+                        float* disagreement /* device [n_units] or NULL */);
+
+/* Saved forward activation of the context, for inspection (device pointer
+ * into the workspace).  which: 0 = block input x (f32), 1 = LN1 out (bf16),
+ * 2 = qkv (bf16), 3 = attention probabilities (bf16), 4 = attention output
+ * (bf16), 5 = residual after attention (f32), 6 = LN2 out (bf16), 7 = MLP
+ * pre-activation (bf16), 8 = GELU out (bf16), 9 = final LN out (bf16),
+ * 10 = logit gradient (bf16), 11 = final residual (f32).  layer is the
+ * block index for 0..8.  dtype_out: 0 = f32, 1 = bf16. */
+layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, const void** ptr,
+                              int64_t* numel, int32_t* dtype_out);
+
+/* ------------------------------------------------------------- raw GEMM */
+
+/* C = op(A) op(B) (+ bias[n]) with float32 accumulation, batched.
+ *   a_kmajor = 1: A element (m,k) at A[m*lda + k]   (rows of A contiguous in k)
+ *   a_kmajor = 0: A element (m,k) at A[k*lda + m]
+ *   b_kmajor = 1: B element (k,n) at B[n*ldb + k]
+ *   b_kmajor = 0: B element (k,n) at B[k*ldb + n]
+ *   C element (m,n) at C[m*ldc + n]; c_f32 = 1 stores float32, 0 bfloat16
+ *   (round to nearest even).
+ * Batch z in [0, batch) offsets each operand by (z / inner)*s_outer +
+ * (z % inner)*s_inner elements (inner >= 1).  The dX GEMM of a linear layer
+ * is a_kmajor=1, b_kmajor=0; the dW GEMM a_kmajor=0, b_kmajor=0; the forward
+ * a_kmajor=1, b_kmajor=1.  Contiguous dimensions and leading dimensions must
+ * be multiples of 8 elements and pointers 16-byte aligned.  The float32 path
+ * (layup_gemm_f32, not batched) has the same layout rules with float operands
+ * and no alignment requirement; it always writes float32. */
+typedef struct {
+  int32_t a_kmajor, b_kmajor;
+  int64_t M, N, K;
+  const void* A;
+  int64_t lda;
+  const void* B;
+  int64_t ldb;
+  void* C;
+  int64_t ldc;
+  int32_t c_f32;
+  int32_t batch;
+  int32_t inner;
+  int32_t reserved;
+  const float* bias;
+  int64_t a_outer, a_inner, b_outer, b_inner, c_outer, c_inner;
+  void* workspace;        /* device, optional: float32 split-K partials
+                             (batch 1 only; split-K is chosen only when the
+                             partials fit).  Either way the result is
+                             deterministic; with and without a workspace the
+                             summation order, and so the rounding, differ. */
+  size_t workspace_bytes;
+} layup_gemm_desc;
+
+layup_status layup_gemm_bf16(const layup_gemm_desc* d, void* stream);
+layup_status layup_gemm_f32(const layup_gemm_desc* d, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAYUP_H */

@@ -1,0 +1,506 @@
+// Non-GEMM kernels of the GPT and MLP forward/backward: embedding gather and
+// deterministic scatter, LayerNorm, causal softmax, cross-entropy, column
+// sums (bias gradients), conversions.  All are HBM-bound elementwise or
+// row-reduction kernels; math is float32 in registers, storage as the caller
+// chooses (bf16 activations, f32 residual stream and gradients).  Every
+// reduction has a fixed order, so results are bitwise reproducible.
+#include "layup_internal.h"
+
+namespace layup {
+
+// ------------------------------------------------------------- embedding
+// x[b,t,:] = wte[tokens[b, t], :] + wpe[t, :]; tokens has seq+1 columns.
+// A token outside [0, V) gathers no embedding row (only the position row).
+__global__ void embed_fwd_kernel(const int32_t* tokens, const float* wte, const float* wpe,
+                                 float* x, int T, int d, int V) {
+  const int row = blockIdx.x;  // b*T + t
+  const int b = row / T, t = row % T;
+  const int tok = tokens[(int64_t)b * (T + 1) + t];
+  const bool ok = tok >= 0 && tok < V;
+  const f32x4* e = reinterpret_cast<const f32x4*>(wte + (int64_t)(ok ? tok : 0) * d);
+  const f32x4* p = reinterpret_cast<const f32x4*>(wpe + (int64_t)t * d);
+  f32x4* o = reinterpret_cast<f32x4*>(x + (int64_t)row * d);
+  for (int i = threadIdx.x; i < d / 4; i += blockDim.x) o[i] = ok ? e[i] + p[i] : p[i];
+}
+
+hipError_t launch_embed_fwd(const int32_t* tokens, const float* wte, const float* wpe, float* x,
+                            int B, int T, int d, int V, hipStream_t s) {
+  embed_fwd_kernel<<<B * T, 64, 0, s>>>(tokens, wte, wpe, x, T, d, V);
+  return hipGetLastError();
+}
+
+// Sort the B*T (token, position) pairs by token, then position, in one
+// workgroup (bitonic sort of packed 32-bit keys token<<14 | position in LDS).
+// Positions with the same token are then contiguous and in increasing order.
+constexpr int SORT_MAX = 8192;
+// Tokens outside [0, V) get the sentinel V and are skipped by the scatter.
+__global__ __launch_bounds__(1024) void token_sort_kernel(const int32_t* tokens, int B, int T,
+                                                          int V, uint32_t* sorted) {
+  __shared__ uint32_t key[SORT_MAX];
+  const int n = B * T;
+  int np = 1;
+  while (np < n) np <<= 1;
+  for (int i = threadIdx.x; i < np; i += blockDim.x) {
+    if (i < n) {
+      int b = i / T, t = i % T;
+      int tok = tokens[(int64_t)b * (T + 1) + t];
+      if (tok < 0 || tok >= V) tok = V;
+      key[i] = ((uint32_t)tok << 14) | (uint32_t)i;
+    } else {
+      key[i] = 0xffffffffu;
+    }
+  }
+  __syncthreads();
+  for (int k = 2; k <= np; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < np; i += blockDim.x) {
+        int ixj = i ^ j;
+        if (ixj > i) {
+          uint32_t a = key[i], c = key[ixj];
+          bool up = (i & k) == 0;
+          if ((a > c) == up) {
+            key[i] = c;
+            key[ixj] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int i = threadIdx.x; i < n; i += blockDim.x) sorted[i] = key[i];
+}
+
+hipError_t launch_token_sort(const int32_t* tokens, int B, int T, int V, int32_t* counts,
+                             int32_t* sorted_pos, int32_t* seg_start, int32_t* seg_token,
+                             int32_t* n_seg, hipStream_t s) {
+  (void)counts; (void)seg_start; (void)seg_token; (void)n_seg;
+  if (B * T > SORT_MAX || V >= (1 << 17)) return hipErrorInvalidValue;
+  token_sort_kernel<<<1, 1024, 0, s>>>(tokens, B, T, V, reinterpret_cast<uint32_t*>(sorted_pos));
+  return hipGetLastError();
+}
+
+// dwte[token] += sum over that token's positions (increasing) of dx[pos];
+// one block per sorted slot, active only at the first slot of a token.
+// dwpe[t] = sum over b (increasing) of dx[b, t]: blocks N.. N+T-1.
+__global__ void embed_bwd_kernel(const float* dx, const uint32_t* sorted, float* dwte,
+                                 float* dwpe, int B, int T, int d, int V) {
+  const int n = B * T;
+  const int i = blockIdx.x;
+  if (i < n) {
+    const uint32_t tok = sorted[i] >> 14;
+    if (tok >= (uint32_t)V) return;
+    if (i > 0 && (sorted[i - 1] >> 14) == tok) return;
+    for (int c = threadIdx.x; c < d / 4; c += blockDim.x) {
+      f32x4 acc = reinterpret_cast<const f32x4*>(dwte + (int64_t)tok * d)[c];
+      for (int j = i; j < n && (sorted[j] >> 14) == tok; ++j) {
+        const int pos = sorted[j] & 0x3fff;
+        acc += reinterpret_cast<const f32x4*>(dx + (int64_t)pos * d)[c];
+      }
+      reinterpret_cast<f32x4*>(dwte + (int64_t)tok * d)[c] = acc;
+    }
+  } else {
+    const int t = i - n;
+    for (int c = threadIdx.x; c < d / 4; c += blockDim.x) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int b = 0; b < B; ++b) acc += reinterpret_cast<const f32x4*>(dx + ((int64_t)b * T + t) * d)[c];
+      reinterpret_cast<f32x4*>(dwpe + (int64_t)t * d)[c] = acc;
+    }
+  }
+}
+
+hipError_t launch_embed_bwd(const float* dx, const int32_t* sorted_pos, float* dwte, float* dwpe,
+                            int B, int T, int d, int V, hipStream_t s) {
+  embed_bwd_kernel<<<B * T + T, 64, 0, s>>>(dx, reinterpret_cast<const uint32_t*>(sorted_pos), dwte,
+                                            dwpe, B, T, d, V);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- LayerNorm
+// One wave64 per row, 4 rows per block.  y = (x - mean) * rstd * g + b in
+// bf16; mean and rstd (1/sqrt(var + 1e-5), biased variance) kept for the
+// backward.
+__global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, const float* g,
+                                                            const float* b, bf16_t* y,
+                                                            float* mean, float* rstd,
+                                                            int64_t rows, int d) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * d);
+  const int nv = d / 4;
+  float s = 0.f;
+  for (int i = lane; i < nv; i += 64) {
+    f32x4 v = xr[i];
+    s += (v[0] + v[1]) + (v[2] + v[3]);
+  }
+  const float mu = warp_sum(s) / d;
+  float ss = 0.f;
+  for (int i = lane; i < nv; i += 64) {
+    f32x4 v = xr[i];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float c = v[j] - mu;
+      ss = fmaf(c, c, ss);
+    }
+  }
+  const float var = warp_sum(ss) / d;
+  const float r = 1.0f / sqrtf(var + 1e-5f);
+  for (int i = lane; i < nv; i += 64) {
+    f32x4 v = xr[i];
+    f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
+    f32x4 bb = reinterpret_cast<const f32x4*>(b)[i];
+    u32x2 o;
+    o[0] = pack_bf2((v[0] - mu) * r * gg[0] + bb[0], (v[1] - mu) * r * gg[1] + bb[1]);
+    o[1] = pack_bf2((v[2] - mu) * r * gg[2] + bb[2], (v[3] - mu) * r * gg[3] + bb[3]);
+    reinterpret_cast<u32x2*>(y + row * d)[i] = o;
+  }
+  if (lane == 0) {
+    mean[row] = mu;
+    rstd[row] = r;
+  }
+}
+
+hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, bf16_t* y,
+                                float* mean, float* rstd, int64_t rows, int d, hipStream_t s) {
+  layernorm_fwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  return hipGetLastError();
+}
+
+// LayerNorm backward.  dx = dres + r*(dxh - mean(dxh) - xh*mean(dxh*xh)) with
+// xh = (x-mean)*r and dxh = dy*g.  dg and db (column sums of dy*xh and dy)
+// are accumulated per block over LN_ROWS rows in fixed order into partial
+// rows, summed later by a column-sum kernel.
+constexpr int LN_ROWS = 16;
+constexpr int LN_MAXV = 8;  // float4 groups per lane: d <= 2048
+
+__global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, const float* x,
+                                                            const float* mean, const float* rstd,
+                                                            const float* g, const float* dres,
+                                                            float* dx, float* pg, float* pb,
+                                                            int64_t rows, int d) {
+  extern __shared__ f32x4 ln_red[];  // [2][4][nv]
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nv = d / 4;
+  f32x4* red_g = ln_red;
+  f32x4* red_b = ln_red + 4 * nv;
+  f32x4 ag[LN_MAXV], ab[LN_MAXV];
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j) ag[j] = ab[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t r0 = (int64_t)blockIdx.x * LN_ROWS;
+  for (int rr = w; rr < LN_ROWS; rr += 4) {
+    const int64_t row = r0 + rr;
+    if (row >= rows) break;
+    const float mu = mean[row], r = rstd[row];
+    const f32x4* dyr = reinterpret_cast<const f32x4*>(dy + row * d);
+    const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * d);
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < LN_MAXV; ++j) {
+      int i = lane + 64 * j;
+      if (i >= nv) break;
+      f32x4 a = dyr[i], xv = xr[i], gg = reinterpret_cast<const f32x4*>(g)[i];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float xh = (xv[e] - mu) * r;
+        float dxh = a[e] * gg[e];
+        s1 += dxh;
+        s2 = fmaf(dxh, xh, s2);
+        ag[j][e] = fmaf(a[e], xh, ag[j][e]);
+        ab[j][e] += a[e];
+      }
+    }
+    s1 = warp_sum(s1) / d;
+    s2 = warp_sum(s2) / d;
+#pragma unroll
+    for (int j = 0; j < LN_MAXV; ++j) {
+      int i = lane + 64 * j;
+      if (i >= nv) break;
+      f32x4 a = dyr[i], xv = xr[i], gg = reinterpret_cast<const f32x4*>(g)[i];
+      f32x4 o = dres ? reinterpret_cast<const f32x4*>(dres + row * d)[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float xh = (xv[e] - mu) * r;
+        o[e] += r * (a[e] * gg[e] - s1 - xh * s2);
+      }
+      reinterpret_cast<f32x4*>(dx + row * d)[i] = o;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < LN_MAXV; ++j) {
+    int i = lane + 64 * j;
+    if (i < nv) {
+      red_g[w * nv + i] = ag[j];
+      red_b[w * nv + i] = ab[j];
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nv; i += 256) {
+    f32x4 sg = red_g[i], sb = red_b[i];
+    for (int k = 1; k < 4; ++k) {
+      sg += red_g[k * nv + i];
+      sb += red_b[k * nv + i];
+    }
+    reinterpret_cast<f32x4*>(pg + (int64_t)blockIdx.x * d)[i] = sg;
+    reinterpret_cast<f32x4*>(pb + (int64_t)blockIdx.x * d)[i] = sb;
+  }
+}
+
+hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
+                                const float* rstd, const float* g, const float* dres, float* dx,
+                                float* pg, float* pb, float* dg, float* db, int64_t rows, int d,
+                                hipStream_t s) {
+  if (d / 4 > LN_MAXV * 64) return hipErrorInvalidValue;
+  const unsigned nb = (unsigned)cdiv(rows, LN_ROWS);
+  const size_t lds = (size_t)2 * 4 * (d / 4) * sizeof(f32x4);
+  layernorm_bwd_kernel<<<nb, 256, lds, s>>>(dy, x, mean, rstd, g, dres, dx, pg, pb, rows, d);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_colsum_f32(pg, nb, d, d, nullptr, dg, s);
+  if (e != hipSuccess) return e;
+  return launch_colsum_f32(pb, nb, d, d, nullptr, db, s);
+}
+
+// ------------------------------------------------------------ column sums
+// out[c] = sum over rows r (increasing, in chunks of CS_ROWS then chunks in
+// increasing order) of x[r*ld + c].
+constexpr int CS_ROWS = 256;
+
+__global__ void colsum_bf16_kernel(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                                   float* partial) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  const int64_t r0 = (int64_t)blockIdx.y * CS_ROWS;
+  const int64_t r1 = min(rows, r0 + CS_ROWS);
+  float s = 0.f;
+  for (int64_t r = r0; r < r1; ++r) s += bf2f(x[r * ld + c]);
+  partial[(int64_t)blockIdx.y * cols + c] = s;
+}
+
+__global__ void colsum_f32_kernel(const float* x, int64_t rows, int64_t cols, int64_t ld,
+                                  float* partial) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  const int64_t r0 = (int64_t)blockIdx.y * CS_ROWS;
+  const int64_t r1 = min(rows, r0 + CS_ROWS);
+  float s = 0.f;
+  for (int64_t r = r0; r < r1; ++r) s += x[r * ld + c];
+  partial[(int64_t)blockIdx.y * cols + c] = s;
+}
+
+__global__ void colsum_final_kernel(const float* partial, int64_t chunks, int64_t cols, float* out) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.f;
+  for (int64_t k = 0; k < chunks; ++k) s += partial[k * cols + c];
+  out[c] = s;
+}
+
+hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              float* partial, float* out, hipStream_t s) {
+  const int64_t chunks = cdiv(rows, CS_ROWS);
+  dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
+  colsum_bf16_kernel<<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, chunks, cols, out);
+  return hipGetLastError();
+}
+
+// With partial == nullptr the input rows are already the partials: one pass.
+hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
+                             float* partial, float* out, hipStream_t s) {
+  if (!partial) {
+    if (ld != cols) return hipErrorInvalidValue;
+    colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(x, rows, cols, out);
+    return hipGetLastError();
+  }
+  const int64_t chunks = cdiv(rows, CS_ROWS);
+  dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
+  colsum_f32_kernel<<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, chunks, cols, out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- causal softmax
+// P[i, j] = exp(scale*S[i,j] - max) / sum for j <= i, 0 for j > i.
+// One wave64 per row.
+__global__ __launch_bounds__(256) void softmax_fwd_kernel(const float* S, bf16_t* P,
+                                                          int64_t n_rows, int T, float scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int i = (int)(row % T);
+  const float* s = S + row * T;
+  bf16_t* p = P + row * T;
+  float mx = -INFINITY;
+  for (int j = lane; j <= i; j += 64) mx = fmaxf(mx, s[j] * scale);
+  mx = warp_max(mx);
+  float sum = 0.f;
+  for (int j = lane; j <= i; j += 64) sum += expf(s[j] * scale - mx);
+  sum = warp_sum(sum);
+  const float inv = 1.0f / sum;
+  for (int j = lane; j < T; j += 64) p[j] = j <= i ? f2bf(expf(s[j] * scale - mx) * inv) : (bf16_t)0;
+}
+
+hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
+                              hipStream_t s) {
+  const int64_t rows = n_mat * T;
+  softmax_fwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(S, P, rows, T, scale);
+  return hipGetLastError();
+}
+
+// dS[i, j] = scale * P[i,j] * (dP[i,j] - sum_k dP[i,k] P[i,k]); zero above
+// the diagonal (P is zero there).
+__global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* dP, const bf16_t* P,
+                                                          bf16_t* dS, int64_t n_rows, int T,
+                                                          float scale) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;
+  const int i = (int)(row % T);
+  const float* dp = dP + row * T;
+  const bf16_t* p = P + row * T;
+  bf16_t* ds = dS + row * T;
+  float acc = 0.f;
+  for (int j = lane; j <= i; j += 64) acc = fmaf(dp[j], bf2f(p[j]), acc);
+  const float D = warp_sum(acc);
+  for (int j = lane; j < T; j += 64)
+    ds[j] = j <= i ? f2bf(scale * bf2f(p[j]) * (dp[j] - D)) : (bf16_t)0;
+}
+
+hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
+                              float scale, hipStream_t s) {
+  const int64_t rows = n_mat * T;
+  softmax_bwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(dP, P, dS, rows, T, scale);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------- cross-entropy
+// Row r = b*T + t of the bf16 logits (logical vocabulary V, storage ld);
+// target tokens[b, t+1].  loss_rows[r] = logsumexp(z) - z[target];
+// dlogits = bf16((softmax(z) - onehot) / (B*T)) for columns < V, 0 beyond.
+__global__ __launch_bounds__(256) void ce_kernel(const bf16_t* z, int64_t ld, const int32_t* tokens,
+                                                 int T, int V, int64_t n_rows, bf16_t* dz,
+                                                 float* loss_rows) {
+  __shared__ float red[16];
+  const int64_t row = blockIdx.x;
+  const int b = (int)(row / T), t = (int)(row % T);
+  int tgt = tokens[(int64_t)b * (T + 1) + t + 1];
+  const bool valid = tgt >= 0 && tgt < V;  // an invalid target adds no loss and no gradient
+  if (!valid) tgt = 0;
+  const bf16_t* zr = z + row * ld;
+  float mx = -INFINITY;
+  for (int j = threadIdx.x; j < V; j += blockDim.x) mx = fmaxf(mx, bf2f(zr[j]));
+  mx = block_max(mx, red);
+  float s = 0.f;
+  for (int j = threadIdx.x; j < V; j += blockDim.x) s += expf(bf2f(zr[j]) - mx);
+  s = block_sum(s, red);
+  const float inv = 1.0f / s;
+  const float scale = 1.0f / (float)n_rows;
+  const float zt = bf2f(zr[tgt]);
+  const float onehot_scale = valid ? 1.0f : 0.0f;
+  __syncthreads();
+  bf16_t* dr = dz + row * ld;
+  for (int j = threadIdx.x; j < ld; j += blockDim.x) {
+    float g = 0.f;
+    if (j < V && valid) g = (expf(bf2f(zr[j]) - mx) * inv - (j == tgt ? onehot_scale : 0.0f)) * scale;
+    dr[j] = f2bf(g);
+  }
+  if (threadIdx.x == 0) loss_rows[row] = valid ? logf(s) + mx - zt : 0.0f;
+}
+
+__global__ void mean_kernel(const float* x, int64_t n, float* out) {
+  __shared__ float red[16];
+  float s = 0.f;
+  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) s += x[i];
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) *out = s / (float)n;
+}
+
+hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B, int T,
+                             int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
+                             hipStream_t s) {
+  const int64_t rows = (int64_t)B * T;
+  ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !loss_out) return e;
+  mean_kernel<<<1, 1024, 0, s>>>(loss_rows, rows, loss_out);
+  return hipGetLastError();
+}
+
+// float32 logits [rows, V] with labels: loss = mean(lse - z[y]),
+// dz = (softmax - onehot) / rows.  One wave64 per row.
+__global__ void ce_f32_kernel(const float* z, const int32_t* labels, int rows, int V, float* dz,
+                              float* loss_rows) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float* zr = z + (int64_t)row * V;
+  float mx = -INFINITY;
+  for (int j = lane; j < V; j += 64) mx = fmaxf(mx, zr[j]);
+  mx = warp_max(mx);
+  float s = 0.f;
+  for (int j = lane; j < V; j += 64) s += expf(zr[j] - mx);
+  s = warp_sum(s);
+  const int y = labels[row];
+  const bool valid = y >= 0 && y < V;  // an invalid label adds no loss and no gradient
+  for (int j = lane; j < V; j += 64)
+    dz[(int64_t)row * V + j] = valid ? (expf(zr[j] - mx) / s - (j == y ? 1.f : 0.f)) / (float)rows : 0.f;
+  if (lane == 0) loss_rows[row] = valid ? logf(s) + mx - zr[y] : 0.f;
+}
+
+hipError_t launch_ce_f32(const float* logits, const int32_t* labels, int rows, int V, float* dlogits,
+                         float* loss_rows, float* loss_out, hipStream_t s) {
+  ce_f32_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(logits, labels, rows, V, dlogits, loss_rows);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !loss_out) return e;
+  mean_kernel<<<1, 256, 0, s>>>(loss_rows, rows, loss_out);
+  return hipGetLastError();
+}
+
+// --------------------------------------------------------- elementwise
+__global__ void f32_to_bf16_kernel(const float* x, bf16_t* y, int64_t n) {
+  const int64_t n4 = n / 4;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    f32x4 v = reinterpret_cast<const f32x4*>(x)[i];
+    u32x2 o;
+    o[0] = pack_bf2(v[0], v[1]);
+    o[1] = pack_bf2(v[2], v[3]);
+    reinterpret_cast<u32x2*>(y)[i] = o;
+  }
+  for (int64_t i = n4 * 4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    y[i] = f2bf(x[i]);
+}
+
+hipError_t launch_f32_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  unsigned blocks = (unsigned)std::min<int64_t>(cdiv(n / 4 + 1, 256), 8192);
+  f32_to_bf16_kernel<<<blocks, 256, 0, s>>>(x, y, n);
+  return hipGetLastError();
+}
+
+__global__ void relu_kernel(float* x, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    x[i] = x[i] > 0.f ? x[i] : 0.f;
+}
+
+__global__ void relu_bwd_kernel(float* dy, const float* y, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    dy[i] = y[i] > 0.f ? dy[i] : 0.f;
+}
+
+hipError_t launch_relu_inplace(float* x, int64_t n, hipStream_t s) {
+  relu_kernel<<<(unsigned)std::min<int64_t>(cdiv(n, 256), 4096), 256, 0, s>>>(x, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_relu_bwd_inplace(float* dy, const float* y, int64_t n, hipStream_t s) {
+  relu_bwd_kernel<<<(unsigned)std::min<int64_t>(cdiv(n, 256), 4096), 256, 0, s>>>(dy, y, n);
+  return hipGetLastError();
+}
+
+}  // namespace layup

@@ -1,0 +1,105 @@
+// Internal declarations shared by the LayUp HIP translation units.
+#pragma once
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+
+#include "../../include/layup.h"
+#include "common.h"
+
+namespace layup {
+
+// ------------------------------------------------------------ update+mix
+constexpr int UM_MAX_TENSORS = 16;
+constexpr int64_t UM_MAX_BLOCKS = 16384;  // grid cap; also the partial-sum scratch size
+
+struct UMTensor {
+  float* p;
+  const float* g;
+  float* m;
+  float* v;
+  const float* q;
+  bf16_t* p16;
+  int64_t n;
+  int32_t decay;
+  int32_t pad;
+};
+
+struct TraceInfo {
+  int32_t* trace = nullptr;
+  int32_t* counter = nullptr;
+  int32_t capacity = 0;
+  int32_t step = 0;
+  int32_t unit = 0;
+};
+
+hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp, float alpha,
+                             float* dis_out, float* dis_partial, const TraceInfo& tr,
+                             hipStream_t stream);
+
+// ------------------------------------------------------------------ GEMM
+enum Epilogue : int {
+  EPI_F32 = 0,    // C(f32) = acc + bias (+ aux residual f32)
+  EPI_BF16 = 1,   // C(bf16) = acc + bias
+  EPI_GELU = 2,   // C(bf16) = acc + bias; C2(bf16) = gelu_tanh(acc + bias)
+  EPI_DGELU = 3,  // C(bf16) = acc * gelu_tanh'(aux bf16)
+};
+
+struct Gemm {
+  bool a_kmajor = true, b_kmajor = true;
+  int64_t M = 0, N = 0, K = 0;
+  const void* A = nullptr;
+  int64_t lda = 0;
+  const void* B = nullptr;
+  int64_t ldb = 0;
+  void* C = nullptr;
+  int64_t ldc = 0;
+  void* C2 = nullptr;         // second output (EPI_GELU)
+  const void* aux = nullptr;  // residual (EPI_F32) or pre-activation (EPI_DGELU), ld = ldc
+  const float* bias = nullptr;
+  int epi = EPI_F32;
+  int batch = 1, inner = 1;
+  int64_t a_outer = 0, a_inner = 0, b_outer = 0, b_inner = 0, c_outer = 0, c_inner = 0;
+  float* splitk_ws = nullptr;  // float32 partials for split-K (batch 1 only)
+  size_t splitk_ws_bytes = 0;
+};
+
+// Validates shapes/alignment; returns a message or empty string.
+std::string gemm_check(const Gemm& g, bool f32_operands);
+hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t stream);
+hipError_t launch_gemm_f32(const Gemm& g, hipStream_t stream);
+
+// ------------------------------------------------------------ glue kernels
+hipError_t launch_embed_fwd(const int32_t* tokens, const float* wte, const float* wpe, float* x,
+                            int B, int T, int d, int V, hipStream_t s);
+hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, bf16_t* y,
+                                float* mean, float* rstd, int64_t rows, int d, hipStream_t s);
+hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
+                                const float* rstd, const float* g, const float* dres,
+                                float* dx, float* dx_partial_g, float* dx_partial_b, float* dg,
+                                float* db, int64_t rows, int d, hipStream_t s);
+hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
+                              hipStream_t s);
+hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
+                              float scale, hipStream_t s);
+hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B,
+                             int T, int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
+                             hipStream_t s);
+hipError_t launch_f32_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s);
+hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              float* partial, float* out, hipStream_t s);
+hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
+                             float* partial, float* out, hipStream_t s);
+hipError_t launch_embed_bwd(const float* dx, const int32_t* sorted_pos, float* dwte, float* dwpe,
+                            int B, int T, int d, int V, hipStream_t s);
+hipError_t launch_token_sort(const int32_t* tokens, int B, int T, int V, int32_t* counts,
+                             int32_t* sorted_pos, int32_t* seg_start, int32_t* seg_token,
+                             int32_t* n_seg, hipStream_t s);
+hipError_t launch_relu_bwd_inplace(float* dy, const float* y, int64_t n, hipStream_t s);
+hipError_t launch_relu_inplace(float* x, int64_t n, hipStream_t s);
+hipError_t launch_ce_f32(const float* logits, const int32_t* labels, int rows, int V,
+                         float* dlogits, float* loss_rows, float* loss_out, hipStream_t s);
+
+}  // namespace layup

@@ -1,0 +1,871 @@
+// The layer-wise LayUp step of one worker and the C ABI around it.
+//
+// Scheduling (LayUp Algorithm 1 and section 3.2): after the forward pass,
+// units are visited from the output back to the input.  Unit u's backward
+// runs on the compute stream and ends by recording the unit's event (the
+// "notify" of Algorithm 1); the update stream waits for that event and runs
+// the fused local update + peer average of unit u while the compute stream
+// already runs unit u-1's backward.  A unit's backward reads only its own
+// weights (which its own update has not touched yet), so the overlap has no
+// hazard; the tied token embedding is updated last because its gradient is
+// complete only after the embedding backward.  The next forward waits for
+// the last update (join).
+//
+// Memory: every parameter-shaped buffer (params, grads, m, v, peers, bf16
+// copy) is one flat caller-owned allocation with the layout built here, so
+// a unit is one or two contiguous ranges and its update is one launch.
+// Activations saved by the forward, gradient scratch and split-K partials
+// live in one caller-owned workspace carved by the context.
+#include <mutex>
+#include <vector>
+
+#include "layup_internal.h"
+
+using namespace layup;
+
+namespace {
+
+thread_local std::string g_err;
+
+struct TensorInfo {
+  std::string name;
+  int64_t off = 0, numel = 0;
+  int rows = 0, cols = 1, padded_rows = 0, unit = 0, decay = 0;
+};
+
+struct Layout {
+  std::vector<TensorInfo> t;
+  int n_units = 0;
+  int64_t total = 0;
+  std::vector<std::vector<int>> unit_tensors;
+};
+
+int64_t align64(int64_t x) { return (x + 63) / 64 * 64; }
+
+std::string check_config(const layup_config& c) {
+  if (c.model == LAYUP_MODEL_MLP_F32) {
+    if (c.n_mlp_layers < 1 || c.n_mlp_layers > LAYUP_MAX_MLP_LAYERS) return "n_mlp_layers out of range";
+    for (int i = 0; i <= c.n_mlp_layers; ++i)
+      if (c.mlp_dims[i] < 1) return "mlp_dims must be positive";
+    if (c.batch < 1) return "batch must be >= 1";
+  } else if (c.model == LAYUP_MODEL_GPT_BF16) {
+    if (c.n_layer < 1 || c.d_model < 8 || c.n_head < 1 || c.d_ff < 8 || c.seq < 1 || c.vocab < 2 ||
+        c.batch < 1)
+      return "GPT dimensions must be positive";
+    if (c.d_model % c.n_head) return "d_model must be a multiple of n_head";
+    if ((c.d_model / c.n_head) % 8) return "head width must be a multiple of 8";
+    if (c.d_model % 8 || c.d_ff % 8 || c.seq % 8) return "d_model, d_ff and seq must be multiples of 8";
+    if (c.d_model > 2048) return "d_model above 2048 is not supported";
+    if ((int64_t)c.batch * c.seq > 8192) return "batch*seq above 8192 is not supported";
+    if (c.vocab >= (1 << 17)) return "vocab must be below 131072";
+  } else {
+    return "unknown model kind";
+  }
+  if (c.n_peers < 1) return "n_peers must be >= 1";
+  return "";
+}
+
+Layout build_layout(const layup_config& c) {
+  Layout L;
+  auto add = [&](const std::string& n, int rows, int cols, int unit, int decay, int padded = 0) {
+    TensorInfo ti;
+    ti.name = n;
+    ti.rows = rows;
+    ti.cols = cols;
+    ti.padded_rows = padded ? padded : rows;
+    ti.numel = (int64_t)rows * cols;
+    ti.unit = unit;
+    ti.decay = decay;
+    ti.off = L.total;
+    L.total = align64(L.total + (int64_t)ti.padded_rows * cols);
+    L.t.push_back(ti);
+  };
+  if (c.model == LAYUP_MODEL_MLP_F32) {
+    L.n_units = c.n_mlp_layers;
+    for (int i = 0; i < c.n_mlp_layers; ++i) {
+      add("fc" + std::to_string(i + 1) + ".w", c.mlp_dims[i + 1], c.mlp_dims[i], i, 1);
+      add("fc" + std::to_string(i + 1) + ".b", c.mlp_dims[i + 1], 1, i, 1);
+    }
+  } else {
+    const int d = c.d_model, f = c.d_ff;
+    L.n_units = c.n_layer + 2;
+    add("wpe", c.seq, d, 0, 1);
+    add("wte", c.vocab, d, 0, 1, (int)align64(c.vocab));
+    for (int l = 0; l < c.n_layer; ++l) {
+      const std::string p = "h" + std::to_string(l) + ".";
+      const int u = l + 1;
+      add(p + "qkv.w", 3 * d, d, u, 1);
+      add(p + "proj.w", d, d, u, 1);
+      add(p + "fc.w", f, d, u, 1);
+      add(p + "mproj.w", d, f, u, 1);
+      add(p + "ln1.g", d, 1, u, 0);
+      add(p + "ln1.b", d, 1, u, 0);
+      add(p + "qkv.b", 3 * d, 1, u, 0);
+      add(p + "proj.b", d, 1, u, 0);
+      add(p + "ln2.g", d, 1, u, 0);
+      add(p + "ln2.b", d, 1, u, 0);
+      add(p + "fc.b", f, 1, u, 0);
+      add(p + "mproj.b", d, 1, u, 0);
+    }
+    add("lnf.g", d, 1, c.n_layer + 1, 0);
+    add("lnf.b", d, 1, c.n_layer + 1, 0);
+  }
+  L.unit_tensors.resize(L.n_units);
+  for (int i = 0; i < (int)L.t.size(); ++i) L.unit_tensors[L.t[i].unit].push_back(i);
+  return L;
+}
+
+// Workspace carving: a bump allocator over the caller's buffer.
+struct Carver {
+  char* base;
+  size_t used = 0;
+  template <class T>
+  T* take(int64_t n) {
+    used = (used + 255) / 256 * 256;
+    T* p = base ? reinterpret_cast<T*>(base + used) : nullptr;
+    used += (size_t)n * sizeof(T);
+    return p;
+  }
+};
+
+struct BlockActs {
+  float *x, *h, *mean1, *rstd1, *mean2, *rstd2;
+  bf16_t *a, *qkv, *P, *o, *a2, *f, *gl;
+};
+
+}  // namespace
+
+struct layup_ctx {
+  layup_config cfg;
+  Layout L;
+  layup_buffers buf;
+  hipStream_t sc = nullptr, su = nullptr;
+  std::vector<hipEvent_t> ev_unit;
+  hipEvent_t ev_join = nullptr;
+  bool have_join = false;
+  std::string err;
+  int device = 0;
+  // state machine of one step
+  bool forward_done = false;
+  int next_backward = -1;
+  std::vector<char> backward_done;
+  int32_t step_index = 0;  // value written to the trace
+  // workspace
+  size_t ws_bytes = 0;
+  std::vector<BlockActs> acts;
+  float *xL = nullptr, *meanf = nullptr, *rstdf = nullptr;
+  bf16_t* xf = nullptr;
+  bf16_t* logits = nullptr;  // logits, then the logit gradient in place
+  float* loss_rows = nullptr;
+  uint32_t* sorted = nullptr;
+  float* S = nullptr;       // scores, then dP
+  bf16_t* dS = nullptr;
+  float* dx[2] = {nullptr, nullptr};
+  float* dh = nullptr;
+  float* da = nullptr;
+  bf16_t *dy16 = nullptr, *df16 = nullptr, *do16 = nullptr, *dqkv16 = nullptr;
+  float *ln_pg = nullptr, *ln_pb = nullptr, *cs_part = nullptr;
+  float* splitk = nullptr;
+  size_t splitk_bytes = 0;
+  float* dis_partial = nullptr;
+  // MLP
+  std::vector<float*> mlp_act;  // input copy not kept: act[0] = x pointer of the step
+  float *mlp_dz = nullptr, *mlp_dh = nullptr;
+  const float* mlp_x = nullptr;
+  const int32_t* tokens = nullptr;
+  int cur_dx = 0;
+};
+
+namespace {
+
+constexpr size_t SPLITK_BYTES = 64u << 20;
+
+size_t carve(layup_ctx* c, char* base) {
+  Carver cv{base};
+  const layup_config& g = c->cfg;
+  if (g.model == LAYUP_MODEL_GPT_BF16) {
+    const int64_t N = (int64_t)g.batch * g.seq, d = g.d_model, F = g.d_ff, H = g.n_head, T = g.seq;
+    const int64_t Vp = align64(g.vocab);
+    c->acts.assign(g.n_layer, BlockActs{});
+    for (int l = 0; l < g.n_layer; ++l) {
+      BlockActs& A = c->acts[l];
+      A.x = cv.take<float>(N * d);
+      A.h = cv.take<float>(N * d);
+      A.mean1 = cv.take<float>(N);
+      A.rstd1 = cv.take<float>(N);
+      A.mean2 = cv.take<float>(N);
+      A.rstd2 = cv.take<float>(N);
+      A.a = cv.take<bf16_t>(N * d);
+      A.qkv = cv.take<bf16_t>(N * 3 * d);
+      A.P = cv.take<bf16_t>(g.batch * H * T * T);
+      A.o = cv.take<bf16_t>(N * d);
+      A.a2 = cv.take<bf16_t>(N * d);
+      A.f = cv.take<bf16_t>(N * F);
+      A.gl = cv.take<bf16_t>(N * F);
+    }
+    c->xL = cv.take<float>(N * d);
+    c->meanf = cv.take<float>(N);
+    c->rstdf = cv.take<float>(N);
+    c->xf = cv.take<bf16_t>(N * d);
+    c->logits = cv.take<bf16_t>(N * Vp);
+    c->loss_rows = cv.take<float>(N);
+    c->sorted = cv.take<uint32_t>(N);
+    c->S = cv.take<float>(g.batch * H * T * T);
+    c->dS = cv.take<bf16_t>(g.batch * H * T * T);
+    c->dx[0] = cv.take<float>(N * d);
+    c->dx[1] = cv.take<float>(N * d);
+    c->dh = cv.take<float>(N * d);
+    c->da = cv.take<float>(N * d);
+    c->dy16 = cv.take<bf16_t>(N * d);
+    c->df16 = cv.take<bf16_t>(N * F);
+    c->do16 = cv.take<bf16_t>(N * d);
+    c->dqkv16 = cv.take<bf16_t>(N * 3 * d);
+    c->ln_pg = cv.take<float>(cdiv(N, 16) * d);
+    c->ln_pb = cv.take<float>(cdiv(N, 16) * d);
+    c->cs_part = cv.take<float>(cdiv(N, 256) * std::max<int64_t>(3 * d, F));
+    c->splitk = cv.take<float>(SPLITK_BYTES / 4);
+    c->splitk_bytes = SPLITK_BYTES;
+  } else {
+    const int n = g.n_mlp_layers;
+    c->mlp_act.assign(n + 1, nullptr);
+    for (int i = 1; i <= n; ++i) c->mlp_act[i] = cv.take<float>((int64_t)g.batch * g.mlp_dims[i]);
+    int64_t wmax = 0;
+    for (int i = 0; i <= n; ++i) wmax = std::max<int64_t>(wmax, g.mlp_dims[i]);
+    c->mlp_dz = cv.take<float>(g.batch * wmax);
+    c->mlp_dh = cv.take<float>(g.batch * wmax);
+    c->loss_rows = cv.take<float>(g.batch);
+    c->cs_part = cv.take<float>(cdiv(g.batch, 256) * wmax);
+  }
+  c->dis_partial = cv.take<float>(UM_MAX_BLOCKS);
+  return cv.used + 256;
+}
+
+layup_status fail(layup_ctx* c, layup_status st, const std::string& msg) {
+  if (c) c->err = msg;
+  g_err = msg;
+  return st;
+}
+
+layup_status hip_fail(layup_ctx* c, hipError_t e, const char* what) {
+  return fail(c, LAYUP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIPCHK(c, expr, what)                     \
+  do {                                            \
+    hipError_t e_ = (expr);                       \
+    if (e_ != hipSuccess) return hip_fail(c, e_, what); \
+  } while (0)
+
+const TensorInfo* find(const layup_ctx* c, const std::string& n) {
+  for (const auto& t : c->L.t)
+    if (t.name == n) return &t;
+  return nullptr;
+}
+
+// pointers into the flat buffers
+struct Flat {
+  layup_ctx* c;
+  float* p(const std::string& n) const { return c->buf.params + find(c, n)->off; }
+  float* g(const std::string& n) const { return c->buf.grads + find(c, n)->off; }
+  bf16_t* w16(const std::string& n) const { return c->buf.params_bf16 + find(c, n)->off; }
+};
+
+Gemm mk(bool ak, bool bk, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
+        int64_t ldb, void* C, int64_t ldc, int epi) {
+  Gemm g;
+  g.a_kmajor = ak;
+  g.b_kmajor = bk;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.lda = lda;
+  g.B = B;
+  g.ldb = ldb;
+  g.C = C;
+  g.ldc = ldc;
+  g.epi = epi;
+  return g;
+}
+
+layup_status run_gemm(layup_ctx* c, Gemm g, hipStream_t s, const char* what) {
+  g.splitk_ws = c->splitk;
+  g.splitk_ws_bytes = c->splitk_bytes;
+  std::string m = gemm_check(g, false);
+  if (!m.empty()) return fail(c, LAYUP_ERR_SHAPE, std::string(what) + ": " + m);
+  HIPCHK(c, launch_gemm_bf16(g, s), what);
+  return LAYUP_OK;
+}
+
+#define TRY(x)                         \
+  do {                                 \
+    layup_status st_ = (x);            \
+    if (st_ != LAYUP_OK) return st_;   \
+  } while (0)
+
+// ---------------------------------------------------------------- GPT
+layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
+  const layup_config& g = c->cfg;
+  const hipStream_t s = c->sc;
+  const int64_t B = g.batch, T = g.seq, N = B * T, d = g.d_model, F = g.d_ff, H = g.n_head,
+                dh = d / H, Vp = align64(g.vocab);
+  const float scale = 1.0f / sqrtf((float)dh);
+  Flat fl{c};
+  HIPCHK(c, launch_embed_fwd(tokens, fl.p("wte"), fl.p("wpe"), c->acts[0].x, (int)B, (int)T, (int)d,
+                             g.vocab, s), "embedding");
+  HIPCHK(c, launch_token_sort(tokens, (int)B, (int)T, g.vocab, nullptr, (int32_t*)c->sorted, nullptr,
+                              nullptr, nullptr, s), "token sort");
+  for (int l = 0; l < g.n_layer; ++l) {
+    BlockActs& A = c->acts[l];
+    const std::string p = "h" + std::to_string(l) + ".";
+    float* x_next = (l + 1 < g.n_layer) ? c->acts[l + 1].x : c->xL;
+    HIPCHK(c, launch_layernorm_fwd(A.x, fl.p(p + "ln1.g"), fl.p(p + "ln1.b"), A.a, A.mean1, A.rstd1,
+                                   N, (int)d, s), "ln1");
+    Gemm q = mk(true, true, N, 3 * d, d, A.a, d, fl.w16(p + "qkv.w"), d, A.qkv, 3 * d, EPI_BF16);
+    q.bias = fl.p(p + "qkv.b");
+    TRY(run_gemm(c, q, s, "qkv forward"));
+    // scores S[z] = Q_h K_h^T, z = b*H + h
+    Gemm sg = mk(true, true, T, T, dh, A.qkv, 3 * d, A.qkv + d, 3 * d, c->S, T, EPI_F32);
+    sg.batch = (int)(B * H);
+    sg.inner = (int)H;
+    sg.a_outer = sg.b_outer = T * 3 * d;
+    sg.a_inner = sg.b_inner = dh;
+    sg.c_outer = H * T * T;
+    sg.c_inner = T * T;
+    TRY(run_gemm(c, sg, s, "scores"));
+    HIPCHK(c, launch_softmax_fwd(c->S, A.P, B * H, (int)T, scale, s), "softmax");
+    // o_h = P V_h
+    Gemm pv = mk(true, false, T, dh, T, A.P, T, A.qkv + 2 * d, 3 * d, A.o, d, EPI_BF16);
+    pv.batch = (int)(B * H);
+    pv.inner = (int)H;
+    pv.a_outer = H * T * T;
+    pv.a_inner = T * T;
+    pv.b_outer = T * 3 * d;
+    pv.b_inner = dh;
+    pv.c_outer = T * d;
+    pv.c_inner = dh;
+    TRY(run_gemm(c, pv, s, "attention output"));
+    Gemm pr = mk(true, true, N, d, d, A.o, d, fl.w16(p + "proj.w"), d, A.h, d, EPI_F32);
+    pr.bias = fl.p(p + "proj.b");
+    pr.aux = A.x;
+    TRY(run_gemm(c, pr, s, "proj forward"));
+    HIPCHK(c, launch_layernorm_fwd(A.h, fl.p(p + "ln2.g"), fl.p(p + "ln2.b"), A.a2, A.mean2, A.rstd2,
+                                   N, (int)d, s), "ln2");
+    Gemm fc = mk(true, true, N, F, d, A.a2, d, fl.w16(p + "fc.w"), d, A.f, F, EPI_GELU);
+    fc.bias = fl.p(p + "fc.b");
+    fc.C2 = A.gl;
+    TRY(run_gemm(c, fc, s, "fc forward"));
+    Gemm mp = mk(true, true, N, d, F, A.gl, F, fl.w16(p + "mproj.w"), F, x_next, d, EPI_F32);
+    mp.bias = fl.p(p + "mproj.b");
+    mp.aux = A.h;
+    TRY(run_gemm(c, mp, s, "mproj forward"));
+  }
+  HIPCHK(c, launch_layernorm_fwd(c->xL, fl.p("lnf.g"), fl.p("lnf.b"), c->xf, c->meanf, c->rstdf, N,
+                                 (int)d, s), "lnf");
+  Gemm hd = mk(true, true, N, Vp, d, c->xf, d, fl.w16("wte"), d, c->logits, Vp, EPI_BF16);
+  TRY(run_gemm(c, hd, s, "head forward"));
+  HIPCHK(c, launch_ce_fwd_bwd(c->logits, Vp, tokens, (int)B, (int)T, g.vocab, c->logits, c->loss_rows,
+                              loss_out, s), "cross-entropy");
+  return LAYUP_OK;
+}
+
+layup_status gpt_backward(layup_ctx* c, int u) {
+  const layup_config& g = c->cfg;
+  const hipStream_t s = c->sc;
+  const int64_t B = g.batch, T = g.seq, N = B * T, d = g.d_model, F = g.d_ff, H = g.n_head,
+                dh = d / H, Vp = align64(g.vocab);
+  const float scale = 1.0f / sqrtf((float)dh);
+  Flat fl{c};
+  if (u == g.n_layer + 1) {
+    // output head (tied wte) and final LayerNorm
+    Gemm dx = mk(true, false, N, d, Vp, c->logits, Vp, fl.w16("wte"), d, c->da, d, EPI_F32);
+    TRY(run_gemm(c, dx, s, "head dX"));
+    Gemm dw = mk(false, false, Vp, d, N, c->logits, Vp, c->xf, d, fl.g("wte"), d, EPI_F32);
+    TRY(run_gemm(c, dw, s, "head dW"));
+    c->cur_dx = 0;
+    HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
+                                   c->dx[0], c->ln_pg, c->ln_pb, fl.g("lnf.g"), fl.g("lnf.b"), N,
+                                   (int)d, s), "lnf backward");
+    return LAYUP_OK;
+  }
+  if (u == 0) {
+    HIPCHK(c, launch_embed_bwd(c->dx[c->cur_dx], (const int32_t*)c->sorted, fl.g("wte"), fl.g("wpe"),
+                               (int)B, (int)T, (int)d, g.vocab, s), "embedding backward");
+    return LAYUP_OK;
+  }
+  const int l = u - 1;
+  const BlockActs& A = c->acts[l];
+  const std::string p = "h" + std::to_string(l) + ".";
+  float* dxo = c->dx[c->cur_dx];
+  float* dxi = c->dx[c->cur_dx ^ 1];
+  // MLP output projection
+  HIPCHK(c, launch_f32_to_bf16(dxo, c->dy16, N * d, s), "dy cast");
+  TRY(run_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32), s,
+               "mproj dW"));
+  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs_part, fl.g(p + "mproj.b"), s), "mproj db");
+  Gemm dg = mk(true, false, N, F, d, c->dy16, d, fl.w16(p + "mproj.w"), F, c->df16, F, EPI_DGELU);
+  dg.aux = A.f;
+  TRY(run_gemm(c, dg, s, "mproj dX + gelu backward"));
+  // MLP input projection
+  TRY(run_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32), s,
+               "fc dW"));
+  HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs_part, fl.g(p + "fc.b"), s), "fc db");
+  TRY(run_gemm(c, mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32), s,
+               "fc dX"));
+  HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
+                                 c->ln_pg, c->ln_pb, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
+                                 s), "ln2 backward");
+  // attention output projection
+  HIPCHK(c, launch_f32_to_bf16(c->dh, c->dy16, N * d, s), "dy2 cast");
+  TRY(run_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32), s,
+               "proj dW"));
+  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs_part, fl.g(p + "proj.b"), s), "proj db");
+  TRY(run_gemm(c, mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16),
+               s, "proj dX"));
+  // attention core, batched over z = b*H + h
+  auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
+                     int64_t ci) {
+    gm.batch = (int)(B * H);
+    gm.inner = (int)H;
+    gm.a_outer = ao;
+    gm.a_inner = ai;
+    gm.b_outer = bo;
+    gm.b_inner = bi;
+    gm.c_outer = co;
+    gm.c_inner = ci;
+    return gm;
+  };
+  const int64_t TT = T * T;
+  // dP = dO_h V_h^T
+  TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
+                          T * d, dh, T * 3 * d, dh, H * TT, TT), s, "dP"));
+  // dV_h = P^T dO_h
+  TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
+                             EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh), s, "dV"));
+  HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
+  // dQ_h = dS K_h
+  TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
+                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh), s, "dQ"));
+  // dK_h = dS^T Q_h
+  TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
+                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh), s, "dK"));
+  // qkv projection
+  TRY(run_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
+                     EPI_F32), s, "qkv dW"));
+  HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs_part, fl.g(p + "qkv.b"), s), "qkv db");
+  TRY(run_gemm(c, mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d,
+                     EPI_F32), s, "qkv dX"));
+  HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
+                                 c->ln_pg, c->ln_pb, fl.g(p + "ln1.g"), fl.g(p + "ln1.b"), N, (int)d,
+                                 s), "ln1 backward");
+  c->cur_dx ^= 1;
+  return LAYUP_OK;
+}
+
+// ---------------------------------------------------------------- MLP
+layup_status mlp_gemm(layup_ctx* c, Gemm g, const char* what) {
+  std::string m = gemm_check(g, true);
+  if (!m.empty()) return fail(c, LAYUP_ERR_SHAPE, std::string(what) + ": " + m);
+  HIPCHK(c, launch_gemm_f32(g, c->sc), what);
+  return LAYUP_OK;
+}
+
+layup_status mlp_forward(layup_ctx* c, const int32_t* labels, const float* x, float* loss_out) {
+  const layup_config& g = c->cfg;
+  const int n = g.n_mlp_layers, Bt = g.batch;
+  Flat fl{c};
+  c->mlp_x = x;
+  const float* h = x;
+  for (int i = 0; i < n; ++i) {
+    const std::string p = "fc" + std::to_string(i + 1) + ".";
+    const int in = g.mlp_dims[i], out = g.mlp_dims[i + 1];
+    Gemm gm = mk(true, true, Bt, out, in, h, in, fl.p(p + "w"), in, c->mlp_act[i + 1], out, EPI_F32);
+    gm.bias = fl.p(p + "b");
+    TRY(mlp_gemm(c, gm, "mlp forward"));
+    if (i + 1 < n) HIPCHK(c, launch_relu_inplace(c->mlp_act[i + 1], (int64_t)Bt * out, c->sc), "relu");
+    h = c->mlp_act[i + 1];
+  }
+  HIPCHK(c, launch_ce_f32(c->mlp_act[n], labels, Bt, g.mlp_dims[n], c->mlp_dz, c->loss_rows, loss_out,
+                          c->sc), "cross-entropy");
+  return LAYUP_OK;
+}
+
+layup_status mlp_backward(layup_ctx* c, int u) {
+  const layup_config& g = c->cfg;
+  const int Bt = g.batch, in = g.mlp_dims[u], out = g.mlp_dims[u + 1];
+  Flat fl{c};
+  const std::string p = "fc" + std::to_string(u + 1) + ".";
+  const float* hin = u == 0 ? c->mlp_x : c->mlp_act[u];
+  TRY(mlp_gemm(c, mk(false, false, out, in, Bt, c->mlp_dz, out, hin, in, fl.g(p + "w"), in, EPI_F32),
+               "mlp dW"));
+  HIPCHK(c, launch_colsum_f32(c->mlp_dz, Bt, out, out, c->cs_part, fl.g(p + "b"), c->sc), "mlp db");
+  if (u > 0) {
+    TRY(mlp_gemm(c, mk(true, false, Bt, in, out, c->mlp_dz, out, fl.p(p + "w"), in, c->mlp_dh, in,
+                       EPI_F32), "mlp dX"));
+    HIPCHK(c, launch_relu_bwd_inplace(c->mlp_dh, c->mlp_act[u], (int64_t)Bt * in, c->sc), "relu bwd");
+    std::swap(c->mlp_dz, c->mlp_dh);
+  }
+  return LAYUP_OK;
+}
+
+// ------------------------------------------------------------ update+mix
+void unit_tensors(layup_ctx* c, int u, int slot, std::vector<UMTensor>& out) {
+  out.clear();
+  const float* peer = c->buf.peers + (int64_t)slot * c->L.total;
+  for (int ti : c->L.unit_tensors[u]) {
+    const TensorInfo& t = c->L.t[ti];
+    if (!out.empty()) {
+      UMTensor& last = out.back();
+      if (last.decay == t.decay && last.p + last.n == c->buf.params + t.off) {
+        last.n += t.numel;
+        continue;
+      }
+    }
+    UMTensor m;
+    m.p = c->buf.params + t.off;
+    m.g = c->buf.grads + t.off;
+    m.m = c->buf.m + t.off;
+    m.v = c->buf.v ? c->buf.v + t.off : nullptr;
+    m.q = peer + t.off;
+    m.p16 = c->buf.params_bf16 ? c->buf.params_bf16 + t.off : nullptr;
+    m.n = t.numel;
+    m.decay = t.decay;
+    m.pad = 0;
+    out.push_back(m);
+  }
+}
+
+std::string check_hp(const layup_hparams* hp) {
+  if (!hp) return "null hparams";
+  if (hp->kind != LAYUP_SGD_MOMENTUM && hp->kind != LAYUP_ADAMW) return "unknown optimizer";
+  if (hp->kind == LAYUP_ADAMW && hp->step < 1) return "AdamW step must be >= 1";
+  if (!std::isfinite(hp->lr) || !std::isfinite(hp->weight_decay)) return "non-finite hyperparameter";
+  return "";
+}
+
+layup_status unit_update(layup_ctx* c, int u, const layup_hparams* hp, float alpha, int slot,
+                         float* dis) {
+  std::string m = check_hp(hp);
+  if (!m.empty()) return fail(c, LAYUP_ERR_INVALID_ARG, m);
+  if (u < 0 || u >= c->L.n_units) return fail(c, LAYUP_ERR_INVALID_ARG, "unit index out of range");
+  if (slot < 0 || slot >= c->cfg.n_peers) return fail(c, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
+  if (hp->kind == LAYUP_ADAMW && !c->buf.v) return fail(c, LAYUP_ERR_INVALID_ARG, "AdamW needs the v buffer");
+  if (!c->backward_done[u]) return fail(c, LAYUP_ERR_STATE, "unit updated before its backward");
+  std::vector<UMTensor> ts;
+  unit_tensors(c, u, slot, ts);
+  HIPCHK(c, hipStreamWaitEvent(c->su, c->ev_unit[u], 0), "wait for unit gradient");
+  TraceInfo tr;
+  tr.trace = c->buf.trace;
+  tr.counter = c->buf.trace_counter;
+  tr.capacity = c->buf.trace_capacity;
+  tr.step = c->step_index;
+  tr.unit = u;
+  for (size_t i = 0; i < ts.size(); i += UM_MAX_TENSORS) {
+    int n = (int)std::min<size_t>(UM_MAX_TENSORS, ts.size() - i);
+    TraceInfo t2 = tr;
+    if (i > 0) t2.trace = nullptr;  // one trace entry per unit
+    HIPCHK(c, launch_update_mix(&ts[i], n, *hp, alpha, (i == 0) ? dis : nullptr, c->dis_partial, t2, c->su),
+           "update+mix");
+  }
+  c->backward_done[u] = 0;
+  if (u == 0) {
+    HIPCHK(c, hipEventRecord(c->ev_join, c->su), "record join");
+    c->have_join = true;
+    c->step_index++;
+  }
+  return LAYUP_OK;
+}
+
+}  // namespace
+
+// ===================================================================== ABI
+extern "C" {
+
+const char* layup_global_error(void) { return g_err.c_str(); }
+
+const char* layup_last_error(const layup_ctx* ctx) { return ctx ? ctx->err.c_str() : g_err.c_str(); }
+
+layup_status layup_param_layout(const layup_config* cfg, int32_t* n_tensors, int32_t* n_units,
+                                int64_t* total) {
+  if (!cfg) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null config");
+  std::string m = check_config(*cfg);
+  if (!m.empty()) return fail(nullptr, LAYUP_ERR_SHAPE, m);
+  Layout L = build_layout(*cfg);
+  if (n_tensors) *n_tensors = (int32_t)L.t.size();
+  if (n_units) *n_units = L.n_units;
+  if (total) *total = L.total;
+  return LAYUP_OK;
+}
+
+layup_status layup_tensor_layout(const layup_config* cfg, int32_t index, layup_tensor_info* out) {
+  if (!cfg || !out) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null argument");
+  std::string m = check_config(*cfg);
+  if (!m.empty()) return fail(nullptr, LAYUP_ERR_SHAPE, m);
+  Layout L = build_layout(*cfg);
+  if (index < 0 || index >= (int)L.t.size()) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "tensor index out of range");
+  const TensorInfo& t = L.t[index];
+  memset(out, 0, sizeof(*out));
+  strncpy(out->name, t.name.c_str(), sizeof(out->name) - 1);
+  out->offset = t.off;
+  out->numel = t.numel;
+  out->rows = t.rows;
+  out->cols = t.cols;
+  out->padded_rows = t.padded_rows;
+  out->unit = t.unit;
+  out->decay = t.decay;
+  return LAYUP_OK;
+}
+
+layup_status layup_workspace_size(const layup_config* cfg, size_t* bytes) {
+  if (!cfg || !bytes) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null argument");
+  std::string m = check_config(*cfg);
+  if (!m.empty()) return fail(nullptr, LAYUP_ERR_SHAPE, m);
+  layup_ctx tmp;
+  tmp.cfg = *cfg;
+  *bytes = carve(&tmp, nullptr);
+  return LAYUP_OK;
+}
+
+layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_buffers* bufs,
+                        void* workspace, size_t workspace_bytes, void* compute_stream,
+                        void* update_stream) {
+  if (!out || !cfg || !bufs || !workspace) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null argument");
+  *out = nullptr;
+  std::string m = check_config(*cfg);
+  if (!m.empty()) return fail(nullptr, LAYUP_ERR_SHAPE, m);
+  if (!bufs->params || !bufs->grads || !bufs->m || !bufs->peers)
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "params, grads, m and peers are required");
+  if (cfg->model == LAYUP_MODEL_GPT_BF16 && !bufs->params_bf16)
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "the GPT model needs the bf16 parameter copy");
+  if (bufs->trace && (!bufs->trace_counter || bufs->trace_capacity < 1))
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "trace needs a counter and a positive capacity");
+  const uintptr_t al = (uintptr_t)bufs->params | (uintptr_t)bufs->grads | (uintptr_t)bufs->m |
+                       (uintptr_t)bufs->v | (uintptr_t)bufs->peers | (uintptr_t)bufs->params_bf16;
+  if (al & 15) return fail(nullptr, LAYUP_ERR_ALIGN, "flat buffers must be 16-byte aligned");
+  if ((uintptr_t)workspace & 255) return fail(nullptr, LAYUP_ERR_ALIGN, "workspace must be 256-byte aligned");
+  layup_ctx* c = new layup_ctx();
+  c->cfg = *cfg;
+  c->L = build_layout(*cfg);
+  c->buf = *bufs;
+  size_t need = carve(c, nullptr);
+  if (workspace_bytes < need) {
+    delete c;
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "workspace smaller than layup_workspace_size");
+  }
+  c->ws_bytes = carve(c, (char*)workspace);
+  c->sc = (hipStream_t)compute_stream;
+  c->su = update_stream ? (hipStream_t)update_stream : c->sc;
+  hipGetDevice(&c->device);
+  c->ev_unit.assign(c->L.n_units, nullptr);
+  c->backward_done.assign(c->L.n_units, 0);
+  for (auto& e : c->ev_unit) {
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      layup_destroy(c);
+      return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
+    }
+  }
+  if (hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
+    layup_destroy(c);
+    return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
+  }
+  *out = c;
+  return LAYUP_OK;
+}
+
+void layup_destroy(layup_ctx* ctx) {
+  if (!ctx) return;
+  for (auto e : ctx->ev_unit)
+    if (e) hipEventDestroy(e);
+  if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
+  delete ctx;
+}
+
+layup_status layup_synchronize(layup_ctx* ctx) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  HIPCHK(ctx, hipStreamSynchronize(ctx->sc), "synchronize compute stream");
+  HIPCHK(ctx, hipStreamSynchronize(ctx->su), "synchronize update stream");
+  return LAYUP_OK;
+}
+
+layup_status layup_refresh_shadow(layup_ctx* ctx) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  if (!ctx->buf.params_bf16) return LAYUP_OK;
+  if (ctx->have_join) HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "wait join");
+  HIPCHK(ctx, launch_f32_to_bf16(ctx->buf.params, ctx->buf.params_bf16, ctx->L.total, ctx->sc),
+         "bf16 copy");
+  return LAYUP_OK;
+}
+
+layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x, float* loss_out) {
+  if (!ctx || !tokens) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null argument");
+  if (ctx->cfg.model == LAYUP_MODEL_MLP_F32 && !x) return fail(ctx, LAYUP_ERR_INVALID_ARG, "the MLP needs x");
+  if (ctx->cfg.model == LAYUP_MODEL_GPT_BF16 && x) return fail(ctx, LAYUP_ERR_INVALID_ARG, "the GPT takes no x");
+  for (char b : ctx->backward_done)
+    if (b) return fail(ctx, LAYUP_ERR_STATE, "forward called while a unit awaits its update");
+  // the forward reads every unit's weights: wait for the previous step's updates
+  if (ctx->have_join) HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "wait join");
+  ctx->tokens = tokens;
+  layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_forward(ctx, tokens, loss_out)
+                                                            : mlp_forward(ctx, tokens, x, loss_out);
+  if (st != LAYUP_OK) return st;
+  ctx->forward_done = true;
+  ctx->next_backward = ctx->L.n_units - 1;
+  return LAYUP_OK;
+}
+
+layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  if (!ctx->forward_done) return fail(ctx, LAYUP_ERR_STATE, "backward before forward");
+  if (unit != ctx->next_backward)
+    return fail(ctx, LAYUP_ERR_STATE, "units must be backpropagated in reverse order, expected " +
+                                          std::to_string(ctx->next_backward));
+  layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_backward(ctx, unit) : mlp_backward(ctx, unit);
+  if (st != LAYUP_OK) return st;
+  HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->sc), "record unit event");
+  ctx->backward_done[unit] = 1;
+  ctx->next_backward--;
+  if (ctx->next_backward < 0) ctx->forward_done = false;
+  return LAYUP_OK;
+}
+
+layup_status layup_unit_update_mix(layup_ctx* ctx, int32_t unit, const layup_hparams* hp, float alpha,
+                                   int32_t peer_slot, float* disagreement) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  return unit_update(ctx, unit, hp, alpha, peer_slot, disagreement);
+}
+
+layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
+                                    const layup_hparams* hp, float alpha, float* disagreement,
+                                    void* stream) {
+  if (!tensors || n_tensors < 1) return fail(ctx, LAYUP_ERR_INVALID_ARG, "no tensors");
+  std::string m = check_hp(hp);
+  if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
+  if (disagreement && !ctx)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output needs a context (its partial sums live in the workspace)");
+  std::vector<UMTensor> ts(n_tensors);
+  for (int i = 0; i < n_tensors; ++i) {
+    const layup_tensor& t = tensors[i];
+    if (!t.param || !t.grad || !t.state0 || !t.peer || t.numel < 0)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": null pointer or negative size");
+    if (hp->kind == LAYUP_ADAMW && !t.state1)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": AdamW needs state1");
+    uintptr_t al = (uintptr_t)t.param | (uintptr_t)t.grad | (uintptr_t)t.state0 | (uintptr_t)t.peer |
+                   (uintptr_t)(hp->kind == LAYUP_ADAMW ? t.state1 : nullptr);
+    if (al & 15) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": pointers must be 16-byte aligned");
+    if ((uintptr_t)t.param_bf16 & 7) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": bf16 copy must be 8-byte aligned");
+    if ((const void*)t.param == (const void*)t.peer || (const void*)t.param == (const void*)t.grad)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": param aliases grad or peer");
+    UMTensor& u = ts[i];
+    u.p = t.param;
+    u.g = t.grad;
+    u.m = t.state0;
+    u.v = hp->kind == LAYUP_ADAMW ? t.state1 : nullptr;
+    u.q = t.peer;
+    u.p16 = t.param_bf16;
+    u.n = t.numel;
+    u.decay = t.decay ? 1 : 0;
+    u.pad = 0;
+  }
+  hipStream_t s = stream ? (hipStream_t)stream : (ctx ? ctx->su : nullptr);
+  TraceInfo tr;
+  float* part = ctx ? ctx->dis_partial : nullptr;
+  if (disagreement && n_tensors > UM_MAX_TENSORS)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
+  for (int i = 0; i < n_tensors; i += UM_MAX_TENSORS) {
+    int n = std::min(UM_MAX_TENSORS, n_tensors - i);
+    hipError_t e = launch_update_mix(&ts[i], n, *hp, alpha, disagreement, part, tr, s);
+    if (e != hipSuccess) return hip_fail(ctx, e, "update+mix");
+  }
+  return LAYUP_OK;
+}
+
+layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x, const layup_hparams* hp,
+                        float alpha, int32_t peer_slot, float* loss_out, float* disagreement) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  std::string m = check_hp(hp);
+  if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
+  if (peer_slot < 0 || peer_slot >= ctx->cfg.n_peers) return fail(ctx, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
+  TRY(layup_forward(ctx, tokens, x, loss_out));
+  for (int u = ctx->L.n_units - 1; u >= 0; --u) {
+    TRY(layup_layer_backward(ctx, u));
+    TRY(unit_update(ctx, u, hp, alpha, peer_slot, disagreement ? disagreement + u : nullptr));
+  }
+  // join: the compute stream continues only after the last update
+  HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "join");
+  return LAYUP_OK;
+}
+
+layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, const void** ptr,
+                              int64_t* numel, int32_t* dtype_out) {
+  if (!ctx || !ptr) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null argument");
+  if (ctx->cfg.model != LAYUP_MODEL_GPT_BF16) return fail(ctx, LAYUP_ERR_DTYPE, "activations are exposed for the GPT model");
+  const layup_config& g = ctx->cfg;
+  const int64_t N = (int64_t)g.batch * g.seq, d = g.d_model, F = g.d_ff;
+  const int64_t PT = (int64_t)g.batch * g.n_head * g.seq * g.seq;
+  if (which <= 8 && (layer < 0 || layer >= g.n_layer)) return fail(ctx, LAYUP_ERR_INVALID_ARG, "layer out of range");
+  const BlockActs* A = which <= 8 ? &ctx->acts[layer] : nullptr;
+  const void* p = nullptr;
+  int64_t n = 0;
+  int dt = 0;
+  switch (which) {
+    case 0: p = A->x; n = N * d; dt = 0; break;
+    case 1: p = A->a; n = N * d; dt = 1; break;
+    case 2: p = A->qkv; n = N * 3 * d; dt = 1; break;
+    case 3: p = A->P; n = PT; dt = 1; break;
+    case 4: p = A->o; n = N * d; dt = 1; break;
+    case 5: p = A->h; n = N * d; dt = 0; break;
+    case 6: p = A->a2; n = N * d; dt = 1; break;
+    case 7: p = A->f; n = N * F; dt = 1; break;
+    case 8: p = A->gl; n = N * F; dt = 1; break;
+    case 9: p = ctx->xf; n = N * d; dt = 1; break;
+    case 10: p = ctx->logits; n = N * align64(g.vocab); dt = 1; break;
+    case 11: p = ctx->xL; n = N * d; dt = 0; break;
+    default: return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown activation");
+  }
+  *ptr = p;
+  if (numel) *numel = n;
+  if (dtype_out) *dtype_out = dt;
+  return LAYUP_OK;
+}
+
+static layup_status gemm_abi(const layup_gemm_desc* d, void* stream, bool f32) {
+  if (!d) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null descriptor");
+  Gemm g;
+  g.a_kmajor = d->a_kmajor != 0;
+  g.b_kmajor = d->b_kmajor != 0;
+  g.M = d->M;
+  g.N = d->N;
+  g.K = d->K;
+  g.A = d->A;
+  g.lda = d->lda;
+  g.B = d->B;
+  g.ldb = d->ldb;
+  g.C = d->C;
+  g.ldc = d->ldc;
+  g.bias = d->bias;
+  g.batch = d->batch < 1 ? 1 : d->batch;
+  g.inner = d->inner < 1 ? 1 : d->inner;
+  g.a_outer = d->a_outer;
+  g.a_inner = d->a_inner;
+  g.b_outer = d->b_outer;
+  g.b_inner = d->b_inner;
+  g.c_outer = d->c_outer;
+  g.c_inner = d->c_inner;
+  g.epi = (f32 || d->c_f32) ? EPI_F32 : EPI_BF16;
+  g.splitk_ws = (float*)d->workspace;
+  g.splitk_ws_bytes = d->workspace_bytes;
+  if (f32 && !d->c_f32) return fail(nullptr, LAYUP_ERR_DTYPE, "the float32 GEMM writes float32");
+  if (f32 && g.batch != 1) return fail(nullptr, LAYUP_ERR_SHAPE, "the float32 GEMM is not batched");
+  if (d->workspace && ((uintptr_t)d->workspace & 15)) return fail(nullptr, LAYUP_ERR_ALIGN, "workspace must be 16-byte aligned");
+  std::string m = gemm_check(g, f32);
+  if (!m.empty()) return fail(nullptr, m.find("aligned") != std::string::npos || m.find("multiple") != std::string::npos
+                                           ? LAYUP_ERR_ALIGN : LAYUP_ERR_SHAPE, m);
+  hipError_t e = f32 ? launch_gemm_f32(g, (hipStream_t)stream) : launch_gemm_bf16(g, (hipStream_t)stream);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "gemm");
+  return LAYUP_OK;
+}
+
+layup_status layup_gemm_bf16(const layup_gemm_desc* d, void* stream) { return gemm_abi(d, stream, false); }
+layup_status layup_gemm_f32(const layup_gemm_desc* d, void* stream) { return gemm_abi(d, stream, true); }
+
+}  // extern "C"

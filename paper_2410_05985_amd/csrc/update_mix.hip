@@ -1,0 +1,182 @@
+// Fused local update + gossip mix, one HBM pass (LayUp Algorithm 1, "Local
+// Update" followed by "Peer Update").
+//
+// Per element, SGD momentum (LibTorch semantics, coupled decay):
+//   g' = g + wd*p;  m = mu*m + g';  p1 = p - lr*m
+// or AdamW (decoupled decay, bias-corrected):
+//   p' = p*(1 - lr*wd);  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g*g;
+//   p1 = p' - (lr/bc1) * m / (sqrt(v)/sqrt(bc2) + eps)
+// then the peer average  p2 = a*p1 + b*q  with a = 1-alpha, b = alpha, and
+// optionally the bfloat16 copy of p2 and the disagreement sum((p1-q)^2).
+//
+// Each tensor is read once and written once: 24 B/param for SGD momentum
+// (read p,g,m,q; write p,m), 32 B/param for AdamW (read p,g,m,v,q; write
+// p,m,v), +2 B with the bfloat16 copy.  Loads and stores are 128-bit; the
+// grid walks (tensor, chunk) pairs of a multi-tensor table so a layer of many
+// small tensors is one launch.
+#include "layup_internal.h"
+
+namespace layup {
+
+constexpr int UM_THREADS = 256;
+constexpr int UM_CHUNK = 4096;  // elements per (block, chunk); multiple of 4*UM_THREADS
+
+struct UMArgs {
+  UMTensor t[UM_MAX_TENSORS];
+  int64_t chunk_prefix[UM_MAX_TENSORS + 1];
+  int32_t n_tensors;
+  int32_t trace_step, trace_unit, trace_cap;
+  float lr, mu, wd, b1, b2, eps, step_size, inv_sqrt_bc2, a, b;
+  float* dis_partial;
+  int32_t* trace;
+  int32_t* trace_counter;
+};
+
+template <int OPT>
+__device__ __forceinline__ void um_elem(float& p, float g, float& m, float& v, float q, float dfac,
+                                        float wdc, const UMArgs& A, float& dis, float& p_out) {
+  float p1;
+  if (OPT == 0) {
+    float gg = fmaf(wdc, p, g);                 // g + wd*p (wdc = 0 without decay)
+    m = fmaf(A.mu, m, gg);
+    p1 = fmaf(-A.lr, m, p);
+  } else {
+    float pd = p * dfac;                        // p * (1 - lr*wd)
+    m = fmaf(A.b1, m, (1.0f - A.b1) * g);
+    v = fmaf(A.b2, v, (1.0f - A.b2) * (g * g));
+    float den = fmaf(sqrtf(v), A.inv_sqrt_bc2, A.eps);
+    p1 = fmaf(-A.step_size, m / den, pd);
+  }
+  float d = p1 - q;
+  dis = fmaf(d, d, dis);
+  p_out = fmaf(A.a, p1, A.b * q);
+}
+
+template <int OPT, bool DIS>
+__global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, int64_t total_chunks) {
+  __shared__ float red[16];
+  float dis = 0.f;
+  for (int64_t c = blockIdx.x; c < total_chunks; c += gridDim.x) {
+    int ti = 0;
+    while (ti + 1 < A.n_tensors && A.chunk_prefix[ti + 1] <= c) ++ti;
+    const UMTensor T = A.t[ti];
+    const int64_t begin = (c - A.chunk_prefix[ti]) * UM_CHUNK;
+    const int64_t end = min(begin + (int64_t)UM_CHUNK, T.n);
+    const float dfac = T.decay ? (1.0f - A.lr * A.wd) : 1.0f;
+    const float wdc = T.decay ? A.wd : 0.0f;
+    const int64_t vend = begin + ((end - begin) & ~(int64_t)3);
+    for (int64_t i = begin + 4 * threadIdx.x; i < vend; i += 4 * UM_THREADS) {
+      f32x4 p = *reinterpret_cast<const f32x4*>(T.p + i);
+      f32x4 g = *reinterpret_cast<const f32x4*>(T.g + i);
+      f32x4 m = *reinterpret_cast<const f32x4*>(T.m + i);
+      f32x4 q = *reinterpret_cast<const f32x4*>(T.q + i);
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (OPT == 1) v = *reinterpret_cast<const f32x4*>(T.v + i);
+      f32x4 po;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float pj = p[j], mj = m[j], vj = v[j], o;
+        um_elem<OPT>(pj, g[j], mj, vj, q[j], dfac, wdc, A, dis, o);
+        m[j] = mj;
+        v[j] = vj;
+        po[j] = o;
+      }
+      *reinterpret_cast<f32x4*>(T.p + i) = po;
+      *reinterpret_cast<f32x4*>(T.m + i) = m;
+      if (OPT == 1) *reinterpret_cast<f32x4*>(T.v + i) = v;
+      if (T.p16) {
+        u32x2 w;
+        w[0] = pack_bf2(po[0], po[1]);
+        w[1] = pack_bf2(po[2], po[3]);
+        *reinterpret_cast<u32x2*>(T.p16 + i) = w;
+      }
+    }
+    // ragged tail of the tensor (fewer than 4 elements)
+    for (int64_t i = vend + threadIdx.x; i < end; i += UM_THREADS) {
+      float p = T.p[i], m = T.m[i], v = OPT == 1 ? T.v[i] : 0.f, o;
+      um_elem<OPT>(p, T.g[i], m, v, T.q[i], dfac, wdc, A, dis, o);
+      T.p[i] = o;
+      T.m[i] = m;
+      if (OPT == 1) T.v[i] = v;
+      if (T.p16) T.p16[i] = f2bf(o);
+    }
+  }
+  if (DIS) {
+    float s = block_sum(dis, red);
+    if (threadIdx.x == 0) A.dis_partial[blockIdx.x] = s;
+  }
+  if (A.trace && blockIdx.x == 0 && threadIdx.x == 0) {
+    int idx = atomicAdd(A.trace_counter, 1);
+    if (idx < A.trace_cap) {
+      A.trace[2 * idx] = A.trace_step;
+      A.trace[2 * idx + 1] = A.trace_unit;
+    }
+  }
+}
+
+// Sum of the per-block partials in block order (deterministic).
+__global__ void sum_partials_kernel(const float* part, int n, float* out) {
+  __shared__ float red[16];
+  float s = 0.f;
+  // each thread sums a strided subset in fixed order, then a fixed tree
+  for (int i = threadIdx.x; i < n; i += blockDim.x) s += part[i];
+  s = block_sum(s, red);
+  if (threadIdx.x == 0) *out = s;
+}
+
+int64_t update_mix_max_blocks() { return UM_MAX_BLOCKS; }
+
+hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp, float alpha,
+                             float* dis_out, float* dis_partial, const TraceInfo& tr,
+                             hipStream_t stream) {
+  UMArgs A;
+  memset(&A, 0, sizeof(A));
+  int64_t chunks = 0;
+  for (int i = 0; i < n; ++i) {
+    A.t[i] = ts[i];
+    A.chunk_prefix[i] = chunks;
+    chunks += cdiv(ts[i].n, UM_CHUNK);
+  }
+  A.chunk_prefix[n] = chunks;
+  A.n_tensors = n;
+  A.lr = hp.lr;
+  A.mu = hp.momentum;
+  A.wd = hp.weight_decay;
+  A.b1 = hp.beta1;
+  A.b2 = hp.beta2;
+  A.eps = hp.eps;
+  if (hp.kind == LAYUP_ADAMW) {
+    double t = (double)hp.step;
+    double bc1 = 1.0 - pow((double)hp.beta1, t);
+    double bc2 = 1.0 - pow((double)hp.beta2, t);
+    A.step_size = (float)((double)hp.lr / bc1);
+    A.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+  }
+  A.a = (float)(1.0 - (double)alpha);
+  A.b = alpha;
+  A.dis_partial = dis_partial;
+  A.trace = tr.trace;
+  A.trace_counter = tr.counter;
+  A.trace_cap = tr.capacity;
+  A.trace_step = tr.step;
+  A.trace_unit = tr.unit;
+  if (chunks == 0) return hipSuccess;
+  int64_t grid = std::min<int64_t>(chunks, UM_MAX_BLOCKS);
+  const bool dis = dis_out != nullptr;
+  if (hp.kind == LAYUP_ADAMW) {
+    if (dis) update_mix_kernel<1, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+    else update_mix_kernel<1, false><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+  } else {
+    if (dis) update_mix_kernel<0, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+    else update_mix_kernel<0, false><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (dis) {
+    sum_partials_kernel<<<1, 1024, 0, stream>>>(dis_partial, (int)grid, dis_out);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+}  // namespace layup

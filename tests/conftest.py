@@ -10,3 +10,12 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+
+
+@pytest.fixture(scope="session")
+def layup_ctx():
+    """A small context whose workspace holds the disagreement partial sums."""
+    from paper_2410_05985_amd import layup as LU
+    m = LU.Model(LU.mlp_config((8, 8), 4), "sgd")
+    yield m.ctx
+    m.close()

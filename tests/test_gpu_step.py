@@ -1,0 +1,287 @@
+"""Parity of the whole layer-wise step (layup_step / layup_forward /
+layup_layer_backward / layup_unit_update_mix) with the oracle: unit order
+(Algorithm 1 loops over layers in backward order; section 3.2 updates a layer
+as soon as its gradient exists), gradients, optimizer state and mixed
+parameters."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2410_05985_amd import synthetic as S
+from tests.parity import compare, compare_chained
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+from paper_2410_05985_amd import layup as LU  # noqa: E402
+
+DEV = "cuda"
+
+
+# ------------------------------------------------------------------ MLP
+
+def mlp_setup(two_streams=True):
+    cfg = S.MLP_TINY
+    x, y = S.mlp_inputs(cfg)
+    params = S.mlp_params(cfg)
+    peer = S.peer_of(params, 0.01)
+    m = LU.Model(LU.mlp_config(cfg.dims, cfg.batch), "sgd", two_streams=two_streams)
+    m.load("params", params)
+    m.load("peers", peer)
+    return cfg, x, y, params, peer, m
+
+
+def test_mlp_ten_steps_parity():
+    """Tiny MLP, float32, SGD momentum 0.9, lr 0.05, alpha 0.5, 10 layer-wise
+    steps chained on both sides.  Tolerance 1e-4 (float32 GEMMs against a
+    float64 reference, compounded over 10 steps; the float64 oracle and an
+    independent float64 torch run agree to 1e-10)."""
+    cfg, x, y, params, peer, m = mlp_setup()
+    hp = LU.hparams("sgd", cfg.lr, cfg.momentum, 0.0)
+    ohp = dict(optim="sgd", lr=cfg.lr, momentum=cfg.momentum, weight_decay=0.0)
+    xd = torch.from_numpy(x).to(DEV)
+    yd = torch.from_numpy(y).to(DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    op = {k: v.astype(np.float64) for k, v in params.items()}
+    om = {k: np.zeros_like(v) for k, v in op.items()}
+    opeer = {k: v.astype(np.float64) for k, v in peer.items()}
+    torch.cuda.synchronize()
+    for s in range(cfg.steps):
+        LU.layup_step(m.ctx, yd[s], xd[s], hp, cfg.alpha, 0, loss)
+        oloss, ograds, otrace, _ = O.mlp_step(op, om, opeer, x[s], y[s], ohp, cfg.alpha)
+        m.synchronize()
+        assert abs(loss.item() - oloss) <= 1e-4 * abs(oloss), (s, loss.item(), oloss)
+        g = m.read("grads")
+        for k in ograds:
+            compare(g[k], ograds[k].reshape(g[k].shape), 1e-4, f"step {s} grad {k}")
+    got = m.read("params")
+    mom = m.read("m")
+    for k in op:
+        compare(got[k], op[k].reshape(got[k].shape), 1e-4, f"param {k}")
+        compare(mom[k], om[k].reshape(mom[k].shape), 1e-4, f"momentum {k}")
+    # order trace: every step visits units 2, 1, 0
+    assert m.read_trace() == [(s, u) for s in range(cfg.steps) for u in (2, 1, 0)]
+    m.close()
+
+
+def test_mlp_two_streams_equal_one_stream():
+    """Overlapping update+mix with the next unit's backward changes timing
+    only: results are bitwise identical to the serialized schedule."""
+    outs = []
+    for two in (True, False):
+        cfg, x, y, params, peer, m = mlp_setup(two)
+        hp = LU.hparams("sgd", cfg.lr, cfg.momentum, 0.0)
+        xd, yd = torch.from_numpy(x).to(DEV), torch.from_numpy(y).to(DEV)
+        torch.cuda.synchronize()
+        for s in range(cfg.steps):
+            LU.layup_step(m.ctx, yd[s], xd[s], hp, cfg.alpha, 0)
+        m.synchronize()
+        outs.append(m.params.cpu().numpy().copy())
+        m.close()
+    assert np.array_equal(outs[0], outs[1])
+
+
+# ------------------------------------------------------------------ GPT
+
+def gpt_setup(cfg, two_streams=True, n_peers=1):
+    params = S.gpt_params(cfg)
+    tokens = S.gpt_tokens(cfg)
+    peers = [S.gpt_peer(cfg, params, slot=i) for i in range(n_peers)]
+    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch,
+                       cfg.vocab, n_peers)
+    m = LU.Model(lc, "adamw", two_streams=two_streams)
+    m.load("params", params)
+    for i, p in enumerate(peers):
+        m.load("peers", p, slot=i)
+    return params, tokens, peers, m
+
+
+def gpt_hp(cfg, step=1):
+    return (LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, step),
+            dict(optim="adamw", lr=cfg.lr, weight_decay=cfg.weight_decay, beta1=cfg.beta1,
+                 beta2=cfg.beta2, eps=cfg.eps))
+
+
+def check_adamw_params(got, ref, g_ref, lr, alpha, name):
+    """After an AdamW step from zero moments the local update is
+    -lr * g/(|g| + eps): where the two sides' gradients agree in sign the
+    mixed parameters agree to 1e-5; where the reference gradient is tiny the
+    bf16 gradient may flip its sign, which moves the step by at most
+    2 lr (1 - alpha) -- both results are valid AdamW steps."""
+    got, ref, g_ref = (np.asarray(a, np.float64) for a in (got, ref, g_ref))
+    rms_g = np.sqrt(np.mean(g_ref ** 2)) if g_ref.size else 0.0
+    firm = np.abs(g_ref) > 0.1 * rms_g
+    if firm.any():
+        compare(got[firm], ref[firm], 1e-5, name + " (firm gradient)")
+    loose = ~firm
+    if loose.any():
+        assert np.all(np.abs(got[loose] - ref[loose]) <= 2 * lr * (1 - alpha) * 1.001
+                      + 1e-5 * (np.abs(ref[loose]) + 1e-3)), name
+
+
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED], ids=lambda c: c.name)
+def test_gpt_forward_activations(cfg):
+    """Saved forward activations against the oracle's forward (bf16 storage
+    points on both sides; chained)."""
+    params, tokens, peers, m = gpt_setup(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    LU.layup_forward(m.ctx, td, None, loss)
+    oloss, dlog, cache = O.gpt_forward({k: v.astype(np.float64) for k, v in params.items()}, tokens,
+                                       cfg.n_head)
+    m.synchronize()
+    assert abs(loss.item() - oloss) <= 2e-3 * abs(oloss)
+    N, d, F = cfg.batch * cfg.seq, cfg.d_model, cfg.d_ff
+    for l in range(cfg.n_layer):
+        c = cache[l]
+        compare_chained(m.activation(0, l).reshape(N, d), c["x"], 2e-2, f"x[{l}]")
+        compare_chained(m.activation(1, l).reshape(N, d), c["a"], 2e-2, f"ln1[{l}]")
+        compare_chained(m.activation(2, l).reshape(N, 3 * d), c["qkv"], 2e-2, f"qkv[{l}]")
+        compare_chained(m.activation(3, l).reshape(c["P"].shape), c["P"], 2e-2, f"P[{l}]")
+        compare_chained(m.activation(4, l).reshape(N, d), c["o"], 2e-2, f"o[{l}]")
+        compare_chained(m.activation(5, l).reshape(N, d), c["h"], 2e-2, f"h[{l}]")
+        compare_chained(m.activation(7, l).reshape(N, F), c["f"], 2e-2, f"f[{l}]")
+        compare_chained(m.activation(8, l).reshape(N, F), c["gl"], 2e-2, f"gelu[{l}]")
+    compare_chained(m.activation(9).reshape(N, d), cache["xf"], 2e-2, "xf")
+    # run the backward so the context is left in a clean state
+    for u in range(m.n_units - 1, -1, -1):
+        LU.layup_layer_backward(m.ctx, u)
+    m.close()
+
+
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED], ids=lambda c: c.name)
+def test_gpt_step_parity(cfg):
+    """One layer-wise step, chained: every gradient at rel 2e-2 (bf16 GEMM
+    operands, float32 accumulation), AdamW moments and the mixed parameters as
+    described in check_adamw_params, order trace exact."""
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, ohp = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    dis = torch.zeros(m.n_units, dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0, loss, dis)
+    op = {k: v.astype(np.float64) for k, v in params.items()}
+    om = {k: np.zeros_like(v) for k, v in op.items()}
+    ov = {k: np.zeros_like(v) for k, v in op.items()}
+    opeer = {k: v.astype(np.float64) for k, v in peers[0].items()}
+    oloss, ograds, otrace, odis = O.gpt_step(op, om, ov, opeer, tokens, cfg.n_head, ohp, cfg.alpha)
+    m.synchronize()
+    assert abs(loss.item() - oloss) <= 2e-3 * abs(oloss)
+    g = m.read("grads")
+    for k, ref in ograds.items():
+        compare_chained(g[k], ref.reshape(g[k].shape), 2e-2, f"grad {k}")
+    got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
+    for k in op:
+        shp = got_p[k].shape
+        check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
+                           f"param {k}")
+        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}")
+        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}")
+    n_units = cfg.n_layer + 2
+    assert otrace == list(range(n_units - 1, -1, -1))
+    assert m.read_trace() == [(0, u) for u in otrace]
+    dgpu = dis.cpu().numpy()
+    for u in range(n_units):
+        assert abs(dgpu[u] - odis[u]) <= 5e-2 * odis[u] + 1e-12, (u, dgpu[u], odis[u])
+    m.close()
+
+
+def test_gpt_two_streams_equal_one_stream_and_repeatable():
+    """Two-stream overlap vs serialized schedule and two identical runs:
+    bitwise identical parameters, moments and gradients (race detector; no
+    float atomics anywhere on the path)."""
+    cfg = S.GPT_TEST
+    outs = []
+    for two in (True, False, True):
+        params, tokens, peers, m = gpt_setup(cfg, two)
+        hp, _ = gpt_hp(cfg)
+        td = torch.from_numpy(tokens).to(DEV)
+        torch.cuda.synchronize()
+        for s in range(2):
+            hp.step = s + 1
+            LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0)
+        m.synchronize()
+        outs.append([t.cpu().numpy().copy() for t in (m.params, m.m, m.v, m.grads)])
+        m.close()
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+    for a, b in zip(outs[0], outs[2]):
+        assert np.array_equal(a, b)
+
+
+def test_gpt_manual_unit_calls_match_step():
+    """Driving forward / backward(u) / update(u) by hand equals layup_step, and
+    out-of-order calls are refused."""
+    cfg = S.GPT_TEST
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, _ = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    torch.cuda.synchronize()
+    with pytest.raises(LU.LayupError) as e:
+        LU.layup_layer_backward(m.ctx, 0)
+    assert e.value.status == LU.LAYUP_ERR_STATE
+    LU.layup_forward(m.ctx, td, None, None)
+    with pytest.raises(LU.LayupError) as e:
+        LU.layup_layer_backward(m.ctx, 0)           # must start at the last unit
+    assert e.value.status == LU.LAYUP_ERR_STATE
+    for u in range(m.n_units - 1, -1, -1):
+        LU.layup_layer_backward(m.ctx, u)
+        LU.layup_unit_update_mix(m.ctx, u, hp, cfg.alpha, 0)
+    m.synchronize()
+    manual = m.params.cpu().numpy().copy()
+    m.close()
+    params, tokens, peers, m2 = gpt_setup(cfg)
+    torch.cuda.synchronize()
+    LU.layup_step(m2.ctx, td, None, hp, cfg.alpha, 0)
+    m2.synchronize()
+    assert np.array_equal(manual, m2.params.cpu().numpy())
+    m2.close()
+
+
+def test_gpt_peer_slots_select_replicas():
+    """With three resident peer replicas, the step mixes with the slot it is
+    given (1.3B workload reading: one peer slot drawn per step)."""
+    cfg = S.GPT_TEST
+    params, tokens, peers, m = gpt_setup(cfg, n_peers=3)
+    hp, ohp = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    torch.cuda.synchronize()
+    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 2)
+    op = {k: v.astype(np.float64) for k, v in params.items()}
+    om = {k: np.zeros_like(v) for k, v in op.items()}
+    ov = {k: np.zeros_like(v) for k, v in op.items()}
+    _, ograds, _, _ = O.gpt_step(op, om, ov, {k: v.astype(np.float64) for k, v in peers[2].items()},
+                                 tokens, cfg.n_head, ohp, cfg.alpha)
+    got = m.read("params")
+    for k in ["lnf.g", "h1.ln2.b", "h0.qkv.w"]:
+        check_adamw_params(got[k], op[k].reshape(got[k].shape), ograds[k].reshape(got[k].shape),
+                           cfg.lr, cfg.alpha, k)
+    m.close()
+
+
+def test_gpt2_small_full_size_step_properties():
+    """GPT-2-small at full size (12 x 768, 12 heads, T 1024, B 8, vocab 50257):
+    the loss at initialisation matches its closed form, every gradient and
+    parameter is finite, the order trace is exact, and the embedding padding
+    rows stay zero.  Closed form: the final LayerNorm output has unit variance
+    per feature and the tied head is N(0, 0.02^2), so the logits are close to
+    Gaussian with variance s2 = d * 0.02^2 and E[logsumexp] = ln V + s2/2."""
+    cfg = S.GPT2_SMALL
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, _ = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0, loss)
+    m.synchronize()
+    expected = math.log(cfg.vocab) + 0.5 * cfg.d_model * 0.02 ** 2
+    assert abs(loss.item() - expected) < 0.02, (loss.item(), expected)
+    assert torch.isfinite(m.grads).all().item() and torch.isfinite(m.params).all().item()
+    assert m.read_trace() == [(0, u) for u in range(13, -1, -1)]
+    wte = m.by_name["wte"]
+    pad = m.params[wte["offset"] + wte["numel"]: wte["offset"] + wte["padded_rows"] * wte["cols"]]
+    assert pad.numel() == 47 * 768 and torch.count_nonzero(pad).item() == 0
+    m.close()

@@ -1,0 +1,151 @@
+"""Parity of the fused update+mix kernel (layup_layer_update_mix) with the
+oracle's local update (Algorithm 1, "Local Update") and peer average
+("Peer Update").  Tolerance: rel 1e-5 for the float32 update+mix; the
+invariants are bit-exact."""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2410_05985_amd import synthetic as S
+from tests.parity import compare
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+from paper_2410_05985_amd import layup as LU  # noqa: E402
+
+DEV = "cuda"
+HP = dict(lr=7.5249e-4, momentum=0.9, weight_decay=0.1, beta1=0.9, beta2=0.95, eps=1e-8)
+
+
+def _hp(optim, step=1, **kw):
+    h = dict(HP, **kw)
+    return LU.hparams(optim, h["lr"], h["momentum"], h["weight_decay"], h["beta1"], h["beta2"],
+                      h["eps"], step)
+
+
+def _ohp(optim, **kw):
+    return dict(HP, optim=optim, **kw)
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def run_gpu(tensors, optim, alpha, step=1, shadow=False, hp_kw=None, dis=False, ctx=None):
+    """tensors: list of (p, g, m, v, q, decay) numpy arrays.  Returns the
+    updated (p, m, v, p16) per tensor and the disagreement."""
+    hp = _hp(optim, step, **(hp_kw or {}))
+    dev, descs = [], []
+    for p, g, m, v, q, decay in tensors:
+        d = dict(p=_dev(p), g=_dev(g), m=_dev(m), v=_dev(v) if v is not None else None, q=_dev(q),
+                 p16=torch.zeros(p.size, dtype=torch.int16, device=DEV) if shadow else None)
+        dev.append(d)
+        descs.append(LU.layup_tensor(param=d["p"].data_ptr(), grad=d["g"].data_ptr(),
+                                     state0=d["m"].data_ptr(),
+                                     state1=d["v"].data_ptr() if d["v"] is not None else None,
+                                     peer=d["q"].data_ptr(),
+                                     param_bf16=d["p16"].data_ptr() if shadow else None,
+                                     numel=p.size, decay=int(decay)))
+    dis_t = torch.zeros(1, dtype=torch.float32, device=DEV) if dis else None
+    torch.cuda.synchronize()
+    LU.layup_layer_update_mix(ctx, descs, hp, alpha, disagreement=dis_t,
+                              stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    out = []
+    for d in dev:
+        p16 = None
+        if shadow:
+            p16 = (d["p16"].to(torch.int32) << 16).view(torch.float32).cpu().numpy()
+        out.append((d["p"].cpu().numpy(), d["m"].cpu().numpy(),
+                    d["v"].cpu().numpy() if d["v"] is not None else None, p16))
+    return out, (float(dis_t.item()) if dis else None)
+
+
+def run_oracle(tensors, optim, alpha, step=1, hp_kw=None):
+    hp = _ohp(optim, **(hp_kw or {}))
+    res, dis = [], 0.0
+    for p, g, m, v, q, decay in tensors:
+        p2, m2, v2, d = O.update_mix(p, g, m, v, q, hp, alpha, step, wd_on=bool(decay))
+        res.append((p2, m2, v2))
+        dis += d
+    return res, dis
+
+
+@pytest.mark.parametrize("optim", ["sgd", "adamw"])
+@pytest.mark.parametrize("n", [1, 3, 4, 7, 4096, 4099, 65541, 1_000_003])
+def test_update_mix_parity_sizes(optim, n):
+    p, g, m, v, q = S.update_mix_inputs(n, 100 + n % 97, optim)
+    t = [(p, g, m, v, q, 1)]
+    step = 3
+    gpu, _ = run_gpu(t, optim, 0.5, step)
+    ref, _ = run_oracle(t, optim, 0.5, step)
+    compare(gpu[0][0], ref[0][0], 1e-5, "p")
+    compare(gpu[0][1], ref[0][1], 1e-5, "m")
+    if optim == "adamw":
+        compare(gpu[0][2], ref[0][2], 1e-5, "v")
+
+
+@pytest.mark.parametrize("optim", ["sgd", "adamw"])
+def test_update_mix_multi_tensor_decay_shadow_disagreement(optim, layup_ctx):
+    """19 tensors (two launches of the 16-tensor table), mixed decay flags,
+    the bf16 copy and the disagreement output."""
+    rng = np.random.default_rng(4)
+    sizes = [int(s) for s in rng.integers(1, 50000, 15)] + [768, 2304, 3, 100_001]
+    tensors = []
+    for i, n in enumerate(sizes):
+        p, g, m, v, q = S.update_mix_inputs(n, 200 + i, optim)
+        tensors.append((p, g, m, v, q, i % 2))
+    gpu, _ = run_gpu(tensors, optim, 0.3, step=2, shadow=True)
+    ref, _ = run_oracle(tensors, optim, 0.3, step=2)
+    for i, ((pg, mg, vg, p16), (pr, mr, vr)) in enumerate(zip(gpu, ref)):
+        compare(pg, pr, 1e-5, f"p[{i}]")
+        compare(mg, mr, 1e-5, f"m[{i}]")
+        if optim == "adamw":
+            compare(vg, vr, 1e-5, f"v[{i}]")
+        # the bf16 copy is the nearest-even bf16 of the stored float32 value
+        assert np.array_equal(p16, O.bf16(pg.astype(np.float64))), i
+    # disagreement: at most 16 tensors per call
+    sub = tensors[:16]
+    _, dis = run_gpu(sub, optim, 0.3, step=2, dis=True, ctx=layup_ctx)
+    _, dref = run_oracle(sub, optim, 0.3, step=2)
+    assert abs(dis - dref) <= 1e-5 * abs(dref), (dis, dref)
+
+
+@pytest.mark.parametrize("optim", ["sgd", "adamw"])
+def test_update_mix_invariants_bit_exact(optim):
+    n = 12345
+    p, g, m, v, q = S.update_mix_inputs(n, 7, optim)
+    # identical peer at lr 0: the layer is unchanged
+    gpu, _ = run_gpu([(p, g, m, v, p.copy(), 1)], optim, 0.5, hp_kw=dict(lr=0.0))
+    assert np.array_equal(gpu[0][0], p)
+    # lr 0: pure average, bit-exact against the oracle
+    gpu, _ = run_gpu([(p, g, m, v, q, 1)], optim, 0.5, hp_kw=dict(lr=0.0))
+    ref, _ = run_oracle([(p, g, m, v, q, 1)], optim, 0.5, hp_kw=dict(lr=0.0))
+    assert np.array_equal(gpu[0][0], ref[0][0])
+    # symmetric pair: both replicas land on the same value (mean preserved)
+    a, _ = run_gpu([(p, g, m, v, q, 1)], optim, 0.5, hp_kw=dict(lr=0.0))
+    b, _ = run_gpu([(q, g, m, v, p, 1)], optim, 0.5, hp_kw=dict(lr=0.0))
+    assert np.array_equal(a[0][0], b[0][0])
+    # alpha 0: the pure optimizer step
+    gpu, _ = run_gpu([(p, g, m, v, q, 1)], optim, 0.0)
+    ref, _ = run_oracle([(p, g, m, v, q, 1)], optim, 0.0)
+    compare(gpu[0][0], ref[0][0], 1e-5, "alpha0")
+
+
+def test_update_mix_gpt2_small_block_full_size():
+    """One GPT-2-small block (7,087,872 parameters) at its real size, AdamW with
+    decoupled decay on the four matrices only, bf16 copy on."""
+    d, f = 768, 3072
+    n_dec = 3 * d * d + d * d + 2 * d * f
+    n_nodec = 7_087_872 - n_dec
+    tensors = []
+    for i, (n, dec) in enumerate([(n_dec, 1), (n_nodec, 0)]):
+        p, g, m, v, q = S.update_mix_inputs(n, 300 + i, "adamw")
+        tensors.append((p, g, m, v, q, dec))
+    gpu, _ = run_gpu(tensors, "adamw", 0.5, step=5, shadow=True)
+    ref, _ = run_oracle(tensors, "adamw", 0.5, step=5)
+    for (pg, mg, vg, _), (pr, mr, vr) in zip(gpu, ref):
+        compare(pg, pr, 1e-5, "p")
+        compare(mg, mr, 1e-5, "m")
+        compare(vg, vr, 1e-5, "v")
