@@ -26,10 +26,8 @@ namespace layup {
 
 namespace {
 
-constexpr int BK = 64;
-constexpr int LDS_PAD = 8;           // bf16 elements of padding per LDS row
-constexpr int LDK = BK + LDS_PAD;    // LDS row stride (elements)
-constexpr int THREADS = 256;
+constexpr int BK = 64;          // K step per LDS stage
+constexpr int THREADS = 256;    // 4 wave64s in a 2x2 grid
 
 struct KArgs {
   const bf16_t* A;
@@ -58,91 +56,134 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
   return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * c * fmaf(3.0f * 0.044715f, x * x, 1.0f);
 }
 
-// Loads of one operand tile (rows x BK) into registers.
-// KMAJOR: element (r, k) at base[r*ld + k]; else at base[k*ld + r].
-template <int ROWS, bool KMAJOR>
-struct TileLoader {
-  // k-major: ROWS*BK/8 vectors of 8 bf16, ROWS/32 per thread
-  // r-major: (BK/4)*(ROWS/8) blocks of 4(k) x 8(r), ROWS/128 per thread (ROWS >= 128)
-  //          or one block per thread for the first 16*ROWS/8 threads (ROWS = 64)
-  static constexpr int NV = KMAJOR ? ROWS / 32 : (ROWS >= 128 ? ROWS / 128 : 1);
-  u32x4 reg[KMAJOR ? NV : NV * 4];
+// ------------------------------------------------------------ pipeline
+// K advances in steps of BKV (32) through a ring of STAGES (4) LDS stages.  Every
+// operand tile is copied HBM -> LDS by direct-to-LDS loads
+// (global_load_lds_dwordx4: each lane's 16 bytes land at LDS base + 16*lane,
+// one 1 KB block per wave instruction), so no registers stage the data and
+// STAGES-1 tiles are in flight while one is multiplied.  Addresses are clamped
+// into the operand (rows >= R read row R-1, k past the end reads the last
+// chunk); rows beyond R only feed discarded outputs and the k tail of the last
+// tile is zeroed in LDS before use.
+//
+// LDS layouts (per tile, byte offsets):
+//  k-major operand, ROWS x 32: row r = 64 B = four 16-byte chunks; chunk c at
+//    r*64 + 16*(c ^ ((r >> 2) & 3)).  Sixteen lanes reading one chunk of 16
+//    consecutive rows (the MFMA operand read, ds_read_b128) cover all banks.
+//  m-major operand, 32 x ROWS (k rows of ROWS elements): chunk c of k-row kk at
+//    kk*2*ROWS + 16*(c ^ sw(kk)), sw(kk) = ((kk & 3) << 2) & (ROWS/8 - 1).  The
+//    operand is read with ds_read_b64_tr_b16: within each 16-lane group, lane
+//    s supplies 4 consecutive m of k-row kb + s/4 and receives, transposed,
+//    4 consecutive k of one m.
+__device__ __forceinline__ constexpr int kswz(int r, int bkv) {
+  // 16 consecutive rows of 2*bkv bytes must cover the 256-byte bank cycle once
+  return (r / (128 / bkv)) % (bkv / 8);
+}
+template <int BKV>
+__device__ __forceinline__ int km_off(int r, int c) { return r * 2 * BKV + 16 * (c ^ kswz(r, BKV)); }
+template <int ROWS>
+__device__ __forceinline__ int mm_sw(int kk) { return ((kk & 3) << 2) & (ROWS / 8 - 1); }
+template <int ROWS>
+__device__ __forceinline__ int mm_off(int kk, int c) { return kk * 2 * ROWS + 16 * (c ^ mm_sw<ROWS>(kk)); }
 
-  __device__ __forceinline__ void load(const bf16_t* base, int64_t ld, int64_t r0, int64_t k0,
-                                       int64_t R, int64_t K, bool guard) {
-    const int t = threadIdx.x;
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+#define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
+
+// Issue this wave's share of the direct-to-LDS copies of one ROWS x BKV tile.
+template <int ROWS, bool KMAJOR, int BKV>
+__device__ __forceinline__ void issue_tile(const bf16_t* base, int64_t ld, int64_t r0, int64_t k0,
+                                           int64_t R, int64_t K, char* lds, int wave, int lane) {
+  constexpr int BLOCKS = ROWS * BKV * 2 / 1024;  // 1 KB blocks per tile
+  constexpr int PER_WAVE = BLOCKS / 4;
+#pragma unroll
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int blk = wave * PER_WAVE + i;
+    const bf16_t* src;
     if (KMAJOR) {
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        int L = t + THREADS * i;
-        int row = L >> 3, kc = (L & 7) * 8;
-        int64_t gr = r0 + row, gk = k0 + kc;
-        if (!guard || (gr < R && gk < K))
-          reg[i] = *reinterpret_cast<const u32x4*>(base + gr * ld + gk);
-        else
-          reg[i] = u32x4{0, 0, 0, 0};
-      }
+      constexpr int KCH = BKV / 8;           // 16-byte chunks per row
+      const int row = blk * (64 / KCH) + lane / KCH;
+      const int c = (lane % KCH) ^ kswz(row, BKV);
+      const int64_t gr = min(r0 + row, R - 1);
+      const int64_t gk = min(k0 + 8 * c, K - 8);
+      src = base + gr * ld + gk;
     } else {
-      constexpr int RG = ROWS / 8;  // 8-wide row groups
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        int L = t + THREADS * i;
-        int rg = L % RG, kg = L / RG;
-        bool active = kg < BK / 4;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          int64_t gk = k0 + kg * 4 + r, gr = r0 + rg * 8;
-          if (active && (!guard || (gk < K && gr < R)))
-            reg[i * 4 + r] = *reinterpret_cast<const u32x4*>(base + gk * ld + gr);
-          else
-            reg[i * 4 + r] = u32x4{0, 0, 0, 0};
-        }
-      }
+      constexpr int LPR = ROWS / 8;           // 16-byte chunks per k-row
+      const int kk = blk * (64 / LPR) + lane / LPR;
+      const int c = (lane % LPR) ^ mm_sw<ROWS>(kk);
+      const int64_t gk = min(k0 + kk, K - 1);
+      const int64_t gm = min(r0 + 8 * c, R - 8);
+      src = base + gk * ld + gm;
+    }
+    __builtin_amdgcn_global_load_lds(src, LDS_PTR(lds + blk * 1024), 16, 0, 0);
+  }
+}
+
+// Zero the k >= krem part of a tile (last, partial K step).
+template <int ROWS, bool KMAJOR, int BKV>
+__device__ __forceinline__ void zero_tail(char* lds, int krem) {
+  if (KMAJOR) {
+    constexpr int KCH = BKV / 8;
+    for (int e = threadIdx.x; e < ROWS * KCH; e += THREADS) {
+      const int r = e / KCH, c = e % KCH;
+      if (8 * c >= krem) *reinterpret_cast<u32x4*>(lds + km_off<BKV>(r, c)) = u32x4{0, 0, 0, 0};
+    }
+  } else {
+    for (int e = threadIdx.x; e < BKV * (ROWS / 8); e += THREADS) {
+      const int kk = e / (ROWS / 8), c = e % (ROWS / 8);
+      if (kk >= krem) *reinterpret_cast<u32x4*>(lds + mm_off<ROWS>(kk, c)) = u32x4{0, 0, 0, 0};
     }
   }
+}
 
-  __device__ __forceinline__ void store(bf16_t* lds) const {
-    const int t = threadIdx.x;
-    if (KMAJOR) {
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        int L = t + THREADS * i;
-        int row = L >> 3, kc = (L & 7) * 8;
-        *reinterpret_cast<u32x4*>(lds + row * LDK + kc) = reg[i];
-      }
-    } else {
-      constexpr int RG = ROWS / 8;
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        int L = t + THREADS * i;
-        int rg = L % RG, kg = L / RG;
-        if (kg >= BK / 4) continue;
-        const u32x4* q = &reg[i * 4];
-#pragma unroll
-        for (int mm = 0; mm < 8; ++mm) {
-          const int w = mm >> 1;
-          uint32_t e0, e1;
-          if (mm & 1) {
-            e0 = (q[0][w] >> 16) | (q[1][w] & 0xffff0000u);
-            e1 = (q[2][w] >> 16) | (q[3][w] & 0xffff0000u);
-          } else {
-            e0 = (q[0][w] & 0xffffu) | (q[1][w] << 16);
-            e1 = (q[2][w] & 0xffffu) | (q[3][w] << 16);
-          }
-          *reinterpret_cast<u32x2*>(lds + (rg * 8 + mm) * LDK + kg * 4) = u32x2{e0, e1};
-        }
-      }
-    }
+// One 32x32x16 MFMA operand fragment: rows rb..rb+31 (lane % 32), k values
+// ks*16 + 8*(lane/32) .. +7 of the tile.
+template <int ROWS, bool KMAJOR, int BKV>
+__device__ __forceinline__ bf16x8 frag(const char* lds, int rb, int ks, int lane) {
+  if (KMAJOR) {
+    const int r = rb + (lane & 31);
+    return *reinterpret_cast<const bf16x8*>(lds + km_off<BKV>(r, 2 * ks + (lane >> 5)));
+  } else {
+    const int g = lane >> 4, s = lane & 15;
+    const int kb = ks * 16 + 8 * (g >> 1) + (s >> 2);
+    const int m = rb + 16 * (g & 1) + 4 * (s & 3);
+    const int c = m >> 3, half = (m & 7) * 2;
+    v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)LDS_PTR(lds + mm_off<ROWS>(kb, c) + half));
+    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4i16*)LDS_PTR(lds + mm_off<ROWS>(kb + 4, c) + half));
+    v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
   }
+}
+
+// s_waitcnt vmcnt(n), expcnt and lgkmcnt left alone (gfx9 encoding).
+#define WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+
+// Workgroup barrier without the release fence of __syncthreads(): the fence
+// would make the compiler drain every outstanding direct-to-LDS load
+// (vmcnt(0)) at each K step; the exact wait is issued by hand before it.
+__device__ __forceinline__ void barrier_only() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int BM, int BN>
+struct TileCfg {
+  static constexpr int BKV = (BM * BN >= 256 * 256) ? 32 : 32;
+  static constexpr int STAGES = 4;
 };
 
 template <int BM, int BN, bool AK, bool BKM, int EPI, bool SPLIT>
-__global__ __launch_bounds__(THREADS, 2) void gemm_bf16_kernel(const KArgs P) {
+__global__ __launch_bounds__(THREADS, (BM * BN > 128 * 128) ? 1 : 2) void gemm_bf16_kernel(const KArgs P) {
+  constexpr int BKV = TileCfg<BM, BN>::BKV, STAGES = TileCfg<BM, BN>::STAGES;
   constexpr int WM = BM / 2, WN = BN / 2;
   constexpr int TM = WM / 32, TN = WN / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * LDK];
-  // buffer b: A tile at smem + b*(BM+BN)*LDK, B tile right after it
-  constexpr int BUF = (BM + BN) * LDK;
+  constexpr int A_BYTES = BM * BKV * 2, STAGE = (BM + BN) * BKV * 2;
+  constexpr int LOADS = (BM + BN) * BKV * 2 / 1024 / 4;  // direct-to-LDS instructions per wave per K step
+  constexpr int KS = BKV / 16;
+  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
   // ---- tile mapping: XCD-aware remap, then group along M
   const int n_tiles = P.tiles_m * P.tiles_n;
@@ -167,7 +208,6 @@ __global__ __launch_bounds__(THREADS, 2) void gemm_bf16_kernel(const KArgs P) {
     kb = split * P.k_per_split;
     ke = min(P.K, kb + P.k_per_split);
   }
-  const bool guard = (m0 + BM > P.M) || (n0 + BN > P.N) || ((ke - kb) % BK != 0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -180,46 +220,56 @@ __global__ __launch_bounds__(THREADS, 2) void gemm_bf16_kernel(const KArgs P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  TileLoader<BM, AK> la;
-  TileLoader<BN, BKM> lb;
-  const int nk = (int)((ke - kb + BK - 1) / BK);
-  if (nk > 0) {
-    la.load(Ab, P.lda, m0, kb, P.M, ke, guard);
-    lb.load(Bb, P.ldb, n0, kb, P.N, ke, guard);
-    la.store(smem);
-    lb.store(smem + BM * LDK);
-  }
-  __syncthreads();
+  const int nk = (int)((ke - kb + BKV - 1) / BKV);
+  const int krem = (int)((ke - kb) - (int64_t)(nk - 1) * BKV);  // valid k in the last step
+  auto issue = [&](int t) {
+    char* st = smem + (t % STAGES) * STAGE;
+    const int64_t k0 = kb + (int64_t)t * BKV;
+    issue_tile<BM, AK, BKV>(Ab, P.lda, m0, k0, P.M, ke, st, wave, lane);
+    issue_tile<BN, BKM, BKV>(Bb, P.ldb, n0, k0, P.N, ke, st + A_BYTES, wave, lane);
+  };
+#pragma unroll
+  for (int t = 0; t < STAGES - 1; ++t)
+    if (t < nk) issue(t);
 
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(Ab, P.lda, m0, kb + (int64_t)(kt + 1) * BK, P.M, ke, guard);
-      lb.load(Bb, P.ldb, n0, kb + (int64_t)(kt + 1) * BK, P.N, ke, guard);
+    // tile kt has landed once at most the loads of the younger tiles are
+    // outstanding; the barrier publishes every wave's copies and frees the
+    // stage that was read in the previous step
+    const int younger = min(STAGES - 2, nk - 1 - kt);
+    if (younger >= 2) WAIT_VMCNT(2 * LOADS);
+    else if (younger == 1) WAIT_VMCNT(LOADS);
+    else WAIT_VMCNT(0);
+    barrier_only();
+    char* st = smem + (kt % STAGES) * STAGE;
+    if (kt == nk - 1 && krem < BKV) {
+      zero_tail<BM, AK, BKV>(st, krem);
+      zero_tail<BN, BKM, BKV>(st + A_BYTES, krem);
+      __syncthreads();
     }
-    const bf16_t* a_s = smem + cur * BUF + (wm * WM + (lane & 31)) * LDK + (lane >> 5) * 8;
-    const bf16_t* b_s = smem + cur * BUF + BM * LDK + (wn * WN + (lane & 31)) * LDK + (lane >> 5) * 8;
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    // operand fragments of sub-step ks+1 are read while the MFMAs of ks run
+    bf16x8 af[2][TM], bfr[2][TN];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[TM], bfr[TN];
+    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK, BKV>(st, wm * WM + i * 32, 0, lane);
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(a_s + i * 32 * LDK + ks * 16);
+    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, BKM, BKV>(st + A_BYTES, wn * WN + j * 32, 0, lane);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(b_s + j * 32 * LDK + ks * 16);
+    for (int ks = 0; ks < KS; ++ks) {
+      const int cb = ks & 1;
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = frag<BM, AK, BKV>(st, wm * WM + i * 32, ks + 1, lane);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfr[cb ^ 1][j] = frag<BN, BKM, BKV>(st + A_BYTES, wn * WN + j * 32, ks + 1, lane);
+      }
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
     }
-    if (more) {
-      la.store(smem + (cur ^ 1) * BUF);
-      lb.store(smem + (cur ^ 1) * BUF + BM * LDK);
-    }
-    __syncthreads();
   }
 
   // ---- epilogue.  32x32 accumulator layout: lane l, register r holds
@@ -293,16 +343,18 @@ __global__ void splitk_reduce_kernel(const KArgs P) {
 template <int BM, int BN, bool AK, bool BKM, int EPI>
 hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   dim3 grid(P.tiles_m * P.tiles_n, P.splits > 1 ? P.splits : batch);
-  if (P.splits > 1) {
-    gemm_bf16_kernel<BM, BN, AK, BKM, EPI, true><<<grid, THREADS, 0, s>>>(P);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    int64_t total = P.M * P.N;
-    int blocks = (int)std::min<int64_t>(cdiv(total, 256), 4096);
-    splitk_reduce_kernel<EPI><<<blocks, 256, 0, s>>>(P);
-  } else {
-    gemm_bf16_kernel<BM, BN, AK, BKM, EPI, false><<<grid, THREADS, 0, s>>>(P);
+  if constexpr (EPI == EPI_F32) {
+    if (P.splits > 1) {
+      gemm_bf16_kernel<BM, BN, AK, BKM, EPI, true><<<grid, THREADS, 0, s>>>(P);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      int64_t total = P.M * P.N;
+      int blocks = (int)std::min<int64_t>(cdiv(total, 256), 4096);
+      splitk_reduce_kernel<EPI><<<blocks, 256, 0, s>>>(P);
+      return hipGetLastError();
+    }
   }
+  gemm_bf16_kernel<BM, BN, AK, BKM, EPI, false><<<grid, THREADS, 0, s>>>(P);
   return hipGetLastError();
 }
 
@@ -311,7 +363,7 @@ hipError_t dispatch_layout(const Gemm& g, const KArgs& P, hipStream_t s) {
   if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, true, true, EPI>(P, g.batch, s);
   if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, true, false, EPI>(P, g.batch, s);
   if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, false, false, EPI>(P, g.batch, s);
-  return launch_tiles<BM, BN, false, true, EPI>(P, g.batch, s);
+  return hipErrorInvalidValue;  // m-major A with k-major B: no caller needs it
 }
 
 template <int BM, int BN>
@@ -324,31 +376,7 @@ hipError_t dispatch_epi(const Gemm& g, const KArgs& P, hipStream_t s) {
   }
 }
 
-}  // namespace
-
-std::string gemm_check(const Gemm& g, bool f32_operands) {
-  if (g.M < 0 || g.N < 0 || g.K < 0) return "negative GEMM dimension";
-  if (g.batch < 1 || g.inner < 1) return "batch and inner must be >= 1";
-  if (!g.A || !g.B || !g.C) return "null GEMM operand";
-  if (g.epi == EPI_GELU && !g.C2) return "GELU epilogue needs a second output";
-  if (g.epi == EPI_DGELU && !g.aux) return "GELU-backward epilogue needs the pre-activation";
-  const int64_t a_contig0 = g.a_kmajor ? g.K : g.M;
-  const int64_t b_contig0 = g.b_kmajor ? g.K : g.N;
-  if (g.lda < a_contig0 || g.ldb < b_contig0 || g.ldc < g.N) return "leading dimension smaller than the row";
-  if (f32_operands) return "";  // scalar loads: no alignment rules
-  const int64_t q = 8;
-  // contiguous dimension of each operand and all leading dims multiples of q
-  const int64_t a_contig = g.a_kmajor ? g.K : g.M;
-  const int64_t b_contig = g.b_kmajor ? g.K : g.N;
-  if (a_contig % q || b_contig % q) return "contiguous GEMM dimensions must be multiples of 8 (bf16) / 4 (f32)";
-  if (g.lda % q || g.ldb % q) return "leading dimensions of A and B must be multiples of 8 (bf16) / 4 (f32)";
-  if (((uintptr_t)g.A | (uintptr_t)g.B) & 15) return "A and B must be 16-byte aligned";
-  if ((g.a_outer | g.a_inner | g.b_outer | g.b_inner) % q) return "batch strides must keep 16-byte alignment";
-  return "";
-}
-
-hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
-  if (g.M == 0 || g.N == 0) return hipSuccess;
+KArgs make_args(const Gemm& g) {
   KArgs P;
   memset(&P, 0, sizeof(P));
   P.A = (const bf16_t*)g.A;
@@ -371,24 +399,81 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   P.c_inner = g.c_inner;
   P.inner = g.inner;
   P.splits = 1;
-  const bool narrow = g.N <= 64;
-  const int BM = 128, BN = narrow ? 64 : 128;
+  return P;
+}
+
+}  // namespace
+
+// Tile configurations: 0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 128x64.
+hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  static const int BMs[] = {256, 256, 128, 128, 128}, BNs[] = {256, 128, 256, 128, 64};
+  KArgs P = make_args(g);
+  const int BM = BMs[cfg], BN = BNs[cfg];
   P.tiles_m = (int)cdiv(g.M, BM);
   P.tiles_n = (int)cdiv(g.N, BN);
-  const int64_t tiles = (int64_t)P.tiles_m * P.tiles_n * g.batch;
-  // split-K when the output tiles cannot fill the machine and K is long
-  if (g.batch == 1 && tiles < 240 && g.K >= 1024 && g.splitk_ws) {
-    int splits = (int)std::min<int64_t>(std::max<int64_t>(1, 512 / tiles), g.K / 512);
+  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32) {
     while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
     if (splits > 1) {
-      P.splits = splits;
       P.k_per_split = cdiv(cdiv(g.K, splits), BK) * BK;
       P.splits = (int)cdiv(g.K, P.k_per_split);
       P.partial = g.splitk_ws;
     }
   }
-  if (narrow) return dispatch_epi<128, 64>(g, P, s);
-  return dispatch_epi<128, 128>(g, P, s);
+  switch (cfg) {
+    case 0: return dispatch_epi<256, 256>(g, P, s);
+    case 1: return dispatch_epi<256, 128>(g, P, s);
+    case 2: return dispatch_epi<128, 256>(g, P, s);
+    case 3: return dispatch_epi<128, 128>(g, P, s);
+    default: return dispatch_epi<128, 64>(g, P, s);
+  }
+}
+
+std::string gemm_check(const Gemm& g, bool f32_operands) {
+  if (g.M < 0 || g.N < 0 || g.K < 0) return "negative GEMM dimension";
+  if (!f32_operands && !g.a_kmajor && g.b_kmajor) return "m-major A with k-major B is not supported";
+  if (g.batch < 1 || g.inner < 1) return "batch and inner must be >= 1";
+  if (!g.A || !g.B || !g.C) return "null GEMM operand";
+  if (g.epi == EPI_GELU && !g.C2) return "GELU epilogue needs a second output";
+  if (g.epi == EPI_DGELU && !g.aux) return "GELU-backward epilogue needs the pre-activation";
+  const int64_t a_contig0 = g.a_kmajor ? g.K : g.M;
+  const int64_t b_contig0 = g.b_kmajor ? g.K : g.N;
+  if (g.lda < a_contig0 || g.ldb < b_contig0 || g.ldc < g.N) return "leading dimension smaller than the row";
+  if (f32_operands) return "";  // scalar loads: no alignment rules
+  const int64_t q = 8;
+  // contiguous dimension of each operand and all leading dims multiples of q
+  const int64_t a_contig = g.a_kmajor ? g.K : g.M;
+  const int64_t b_contig = g.b_kmajor ? g.K : g.N;
+  if (a_contig % q || b_contig % q) return "contiguous GEMM dimensions must be multiples of 8 (bf16) / 4 (f32)";
+  if (g.lda % q || g.ldb % q) return "leading dimensions of A and B must be multiples of 8 (bf16) / 4 (f32)";
+  if (((uintptr_t)g.A | (uintptr_t)g.B) & 15) return "A and B must be 16-byte aligned";
+  if ((g.a_outer | g.a_inner | g.b_outer | g.b_inner) % q) return "batch strides must keep 16-byte alignment";
+  return "";
+}
+
+// Tile choice (measured on MI355X): 256x256 pays off only when both output
+// dimensions and K are large; otherwise 128x128 (two workgroups per CU) is
+// faster.  N <= 64 (attention head width) takes 128x64.  Split-K when the
+// output has fewer tiles than CUs and K is long (the dW GEMMs).
+hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  const int64_t cus = 256;
+  auto tiles = [&](int bm, int bn) { return cdiv(g.M, bm) * cdiv(g.N, bn) * g.batch; };
+  int cfg, bm = 128, bn = 128;
+  if (g.N <= 64) {
+    cfg = 4;
+    bn = 64;
+  } else if (tiles(256, 256) >= cus && g.K >= 4096) {
+    cfg = 0;
+    bm = bn = 256;
+  } else {
+    cfg = 3;
+  }
+  int splits = 1;
+  const int64_t t = tiles(bm, bn);
+  if (g.batch == 1 && t < cus && g.K >= 1024)
+    splits = (int)std::min<int64_t>(std::max<int64_t>(1, (2 * cus) / t), g.K / 512);
+  return launch_gemm_bf16_cfg(g, cfg, splits, s);
 }
 
 }  // namespace layup

@@ -247,43 +247,89 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, con
 
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres, float* dx,
-                                float* pg, float* pb, float* dg, float* db, int64_t rows, int d,
-                                hipStream_t s) {
+                                float* pg, float* pb, float* cs_scratch, float* dg, float* db,
+                                int64_t rows, int d, hipStream_t s) {
   if (d / 4 > LN_MAXV * 64) return hipErrorInvalidValue;
   const unsigned nb = (unsigned)cdiv(rows, LN_ROWS);
   const size_t lds = (size_t)2 * 4 * (d / 4) * sizeof(f32x4);
   layernorm_bwd_kernel<<<nb, 256, lds, s>>>(dy, x, mean, rstd, g, dres, dx, pg, pb, rows, d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_colsum_f32(pg, nb, d, d, nullptr, dg, s);
+  e = launch_colsum_f32(pg, nb, d, d, cs_scratch, dg, s);
   if (e != hipSuccess) return e;
-  return launch_colsum_f32(pb, nb, d, d, nullptr, db, s);
+  return launch_colsum_f32(pb, nb, d, d, cs_scratch, db, s);
 }
 
 // ------------------------------------------------------------ column sums
-// out[c] = sum over rows r (increasing, in chunks of CS_ROWS then chunks in
-// increasing order) of x[r*ld + c].
-constexpr int CS_ROWS = 256;
+// out[c] = sum over rows of x[r*ld + c], in a fixed order: stage 1 sums
+// chunks of CS_ROWS rows (inside a chunk: rows r = l, l+8, ... per row lane
+// l, then the 8 row lanes in order), stage 2 sums the chunk partials in chunk
+// order.  Stage 1 reads 16 bytes per thread per row, coalesced across the
+// 32 column groups of a block.
+constexpr int CS_ROWS = 128;
 
-__global__ void colsum_bf16_kernel(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                                   float* partial) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= cols) return;
-  const int64_t r0 = (int64_t)blockIdx.y * CS_ROWS;
-  const int64_t r1 = min(rows, r0 + CS_ROWS);
-  float s = 0.f;
-  for (int64_t r = r0; r < r1; ++r) s += bf2f(x[r * ld + c]);
-  partial[(int64_t)blockIdx.y * cols + c] = s;
+template <typename T>
+__device__ __forceinline__ void load_vec(const T* p, float* out);
+template <>
+__device__ __forceinline__ void load_vec<bf16_t>(const bf16_t* p, float* out) {
+  const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __builtin_bit_cast(float, v[i] << 16);
+    out[2 * i + 1] = __builtin_bit_cast(float, v[i] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void load_vec<float>(const float* p, float* out) {
+  const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = v[i];
 }
 
-__global__ void colsum_f32_kernel(const float* x, int64_t rows, int64_t cols, int64_t ld,
-                                  float* partial) {
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_stage1(const T* x, int64_t rows, int64_t cols, int64_t ld,
+                                                     float* partial) {
+  constexpr int VEC = 16 / sizeof(T);
+  __shared__ float red[8][32 * VEC];
+  const int cg = threadIdx.x & 31, rl = threadIdx.x >> 5;
+  const int64_t c0 = ((int64_t)blockIdx.x * 32 + cg) * VEC;
+  const int64_t r0 = (int64_t)blockIdx.y * CS_ROWS;
+  const int64_t r1 = min(rows, r0 + CS_ROWS);
+  float acc[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+  if (c0 < cols) {
+    for (int64_t r = r0 + rl; r < r1; r += 8) {
+      float v[VEC];
+      load_vec<T>(x + r * ld + c0, v);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += v[e];
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) red[rl][cg * VEC + e] = acc[e];
+  __syncthreads();
+  for (int i = threadIdx.x; i < 32 * VEC; i += 256) {
+    const int64_t c = (int64_t)blockIdx.x * 32 * VEC + i;
+    if (c >= cols) continue;
+    float t = red[0][i];
+    for (int l = 1; l < 8; ++l) t += red[l][i];
+    partial[(int64_t)blockIdx.y * cols + c] = t;
+  }
+}
+
+// Scalar fallback for narrow or unaligned inputs (the float32 MLP's 10 classes).
+template <typename T>
+__global__ void colsum_scalar(const T* x, int64_t rows, int64_t cols, int64_t ld, float* partial) {
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= cols) return;
   const int64_t r0 = (int64_t)blockIdx.y * CS_ROWS;
   const int64_t r1 = min(rows, r0 + CS_ROWS);
   float s = 0.f;
-  for (int64_t r = r0; r < r1; ++r) s += x[r * ld + c];
+  for (int64_t r = r0; r < r1; ++r) {
+    if constexpr (sizeof(T) == 2) s += bf2f(x[r * ld + c]);
+    else s += x[r * ld + c];
+  }
   partial[(int64_t)blockIdx.y * cols + c] = s;
 }
 
@@ -295,64 +341,88 @@ __global__ void colsum_final_kernel(const float* partial, int64_t chunks, int64_
   out[c] = s;
 }
 
-hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              float* partial, float* out, hipStream_t s) {
+template <typename T>
+hipError_t colsum(const T* x, int64_t rows, int64_t cols, int64_t ld, float* partial, float* out,
+                  hipStream_t s) {
+  constexpr int VEC = 16 / sizeof(T);
   const int64_t chunks = cdiv(rows, CS_ROWS);
-  dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
-  colsum_bf16_kernel<<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+  const bool vec = cols % VEC == 0 && ld % VEC == 0 && ((uintptr_t)x & 15) == 0;
+  if (vec) {
+    dim3 g1((unsigned)cdiv(cols, 32 * VEC), (unsigned)chunks);
+    colsum_stage1<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+  } else {
+    dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
+    colsum_scalar<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, chunks, cols, out);
   return hipGetLastError();
 }
 
-// With partial == nullptr the input rows are already the partials: one pass.
+hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                              float* partial, float* out, hipStream_t s) {
+  return colsum<bf16_t>(x, rows, cols, ld, partial, out, s);
+}
+
 hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
                              float* partial, float* out, hipStream_t s) {
-  if (!partial) {
-    if (ld != cols) return hipErrorInvalidValue;
-    colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(x, rows, cols, out);
-    return hipGetLastError();
-  }
-  const int64_t chunks = cdiv(rows, CS_ROWS);
-  dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
-  colsum_f32_kernel<<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, chunks, cols, out);
-  return hipGetLastError();
+  return colsum<float>(x, rows, cols, ld, partial, out, s);
 }
 
 // ------------------------------------------------------- causal softmax
-// P[i, j] = exp(scale*S[i,j] - max) / sum for j <= i, 0 for j > i.
-// One wave64 per row.
+// P[i, j] = exp(scale*S[i,j] - max) / sum for j <= i, 0 for j > i.  One wave64
+// per row; 16-byte loads of S; only the unmasked part of S is read.
 __global__ __launch_bounds__(256) void softmax_fwd_kernel(const float* S, bf16_t* P,
                                                           int64_t n_rows, int T, float scale) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;
   const int i = (int)(row % T);
-  const float* s = S + row * T;
-  bf16_t* p = P + row * T;
+  const f32x4* s = reinterpret_cast<const f32x4*>(S + row * T);
+  u32x2* p = reinterpret_cast<u32x2*>(P + row * T);
+  const int nv = i / 4 + 1;  // vectors holding columns 0..i
   float mx = -INFINITY;
-  for (int j = lane; j <= i; j += 64) mx = fmaxf(mx, s[j] * scale);
+  for (int v = lane; v < nv; v += 64) {
+    const f32x4 x = s[v];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (4 * v + e <= i) mx = fmaxf(mx, x[e] * scale);
+  }
   mx = warp_max(mx);
   float sum = 0.f;
-  for (int j = lane; j <= i; j += 64) sum += expf(s[j] * scale - mx);
+  for (int v = lane; v < nv; v += 64) {
+    const f32x4 x = s[v];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (4 * v + e <= i) sum += expf(x[e] * scale - mx);
+  }
   sum = warp_sum(sum);
   const float inv = 1.0f / sum;
-  for (int j = lane; j < T; j += 64) p[j] = j <= i ? f2bf(expf(s[j] * scale - mx) * inv) : (bf16_t)0;
+  for (int v = lane; v < T / 4; v += 64) {
+    u32x2 o = {0u, 0u};
+    if (v < nv) {
+      const f32x4 x = s[v];
+      float y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = (4 * v + e <= i) ? expf(x[e] * scale - mx) * inv : 0.f;
+      o[0] = pack_bf2(y[0], y[1]);
+      o[1] = pack_bf2(y[2], y[3]);
+    }
+    p[v] = o;
+  }
 }
 
 hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
                               hipStream_t s) {
+  if (T % 4) return hipErrorInvalidValue;
   const int64_t rows = n_mat * T;
   softmax_fwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(S, P, rows, T, scale);
   return hipGetLastError();
 }
 
 // dS[i, j] = scale * P[i,j] * (dP[i,j] - sum_k dP[i,k] P[i,k]); zero above
-// the diagonal (P is zero there).
+// the diagonal (P is zero there).  One wave64 per row, unmasked part read.
 __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* dP, const bf16_t* P,
                                                           bf16_t* dS, int64_t n_rows, int T,
                                                           float scale) {
@@ -360,55 +430,124 @@ __global__ __launch_bounds__(256) void softmax_bwd_kernel(const float* dP, const
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;
   const int i = (int)(row % T);
-  const float* dp = dP + row * T;
-  const bf16_t* p = P + row * T;
-  bf16_t* ds = dS + row * T;
+  const f32x4* dp = reinterpret_cast<const f32x4*>(dP + row * T);
+  const u32x2* p = reinterpret_cast<const u32x2*>(P + row * T);
+  u32x2* ds = reinterpret_cast<u32x2*>(dS + row * T);
+  const int nv = i / 4 + 1;
   float acc = 0.f;
-  for (int j = lane; j <= i; j += 64) acc = fmaf(dp[j], bf2f(p[j]), acc);
+  for (int v = lane; v < nv; v += 64) {
+    const f32x4 g = dp[v];
+    const u32x2 pv = p[v];
+    const float pe[4] = {__builtin_bit_cast(float, pv[0] << 16), __builtin_bit_cast(float, pv[0] & 0xffff0000u),
+                         __builtin_bit_cast(float, pv[1] << 16), __builtin_bit_cast(float, pv[1] & 0xffff0000u)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) acc = fmaf(g[e], pe[e], acc);  // P is 0 beyond the diagonal
+  }
   const float D = warp_sum(acc);
-  for (int j = lane; j < T; j += 64)
-    ds[j] = j <= i ? f2bf(scale * bf2f(p[j]) * (dp[j] - D)) : (bf16_t)0;
+  for (int v = lane; v < T / 4; v += 64) {
+    u32x2 o = {0u, 0u};
+    if (v < nv) {
+      const f32x4 g = dp[v];
+      const u32x2 pv = p[v];
+      const float pe[4] = {__builtin_bit_cast(float, pv[0] << 16), __builtin_bit_cast(float, pv[0] & 0xffff0000u),
+                           __builtin_bit_cast(float, pv[1] << 16), __builtin_bit_cast(float, pv[1] & 0xffff0000u)};
+      float y[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = scale * pe[e] * (g[e] - D);
+      o[0] = pack_bf2(y[0], y[1]);
+      o[1] = pack_bf2(y[2], y[3]);
+    }
+    ds[v] = o;
+  }
 }
 
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
                               float scale, hipStream_t s) {
+  if (T % 4) return hipErrorInvalidValue;
   const int64_t rows = n_mat * T;
   softmax_bwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(dP, P, dS, rows, T, scale);
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------- cross-entropy
-// Row r = b*T + t of the bf16 logits (logical vocabulary V, storage ld);
-// target tokens[b, t+1].  loss_rows[r] = logsumexp(z) - z[target];
+// Row r = b*T + t of the bf16 logits (logical vocabulary V, storage ld, a
+// multiple of 8); target tokens[b, t+1].  loss_rows[r] = logsumexp(z) - z[y];
 // dlogits = bf16((softmax(z) - onehot) / (B*T)) for columns < V, 0 beyond.
+// Pass 1 keeps a running (max, sum of exp) per thread over 16-byte vectors,
+// combined across the block in a fixed order; pass 2 writes the gradient
+// (in place over the logits is allowed: each element is read before it is
+// written, by the same thread).
 __global__ __launch_bounds__(256) void ce_kernel(const bf16_t* z, int64_t ld, const int32_t* tokens,
                                                  int T, int V, int64_t n_rows, bf16_t* dz,
                                                  float* loss_rows) {
-  __shared__ float red[16];
+  __shared__ float rm[4], rs[4];
   const int64_t row = blockIdx.x;
   const int b = (int)(row / T), t = (int)(row % T);
   int tgt = tokens[(int64_t)b * (T + 1) + t + 1];
   const bool valid = tgt >= 0 && tgt < V;  // an invalid target adds no loss and no gradient
   if (!valid) tgt = 0;
-  const bf16_t* zr = z + row * ld;
-  float mx = -INFINITY;
-  for (int j = threadIdx.x; j < V; j += blockDim.x) mx = fmaxf(mx, bf2f(zr[j]));
-  mx = block_max(mx, red);
-  float s = 0.f;
-  for (int j = threadIdx.x; j < V; j += blockDim.x) s += expf(bf2f(zr[j]) - mx);
-  s = block_sum(s, red);
-  const float inv = 1.0f / s;
-  const float scale = 1.0f / (float)n_rows;
-  const float zt = bf2f(zr[tgt]);
-  const float onehot_scale = valid ? 1.0f : 0.0f;
-  __syncthreads();
-  bf16_t* dr = dz + row * ld;
-  for (int j = threadIdx.x; j < ld; j += blockDim.x) {
-    float g = 0.f;
-    if (j < V && valid) g = (expf(bf2f(zr[j]) - mx) * inv - (j == tgt ? onehot_scale : 0.0f)) * scale;
-    dr[j] = f2bf(g);
+  const u32x4* zr = reinterpret_cast<const u32x4*>(z + row * ld);
+  const int nv = (int)(ld / 8);
+  float m = -INFINITY, sum = 0.f;
+  for (int v = threadIdx.x; v < nv; v += blockDim.x) {
+    const u32x4 w = zr[v];
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x[2 * k] = __builtin_bit_cast(float, w[k] << 16);
+      x[2 * k + 1] = __builtin_bit_cast(float, w[k] & 0xffff0000u);
+    }
+    float lm = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (8 * v + e < V) lm = fmaxf(lm, x[e]);
+    if (lm == -INFINITY) continue;
+    const float mn = fmaxf(m, lm);
+    float acc = sum * expf(m - mn);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (8 * v + e < V) acc += expf(x[e] - mn);
+    m = mn;
+    sum = acc;
   }
-  if (threadIdx.x == 0) loss_rows[row] = valid ? logf(s) + mx - zt : 0.0f;
+  // combine (m, sum) across lanes, then across the four waves, in fixed order
+  for (int o = 32; o > 0; o >>= 1) {
+    const float om = __shfl_xor(m, o, 64), os = __shfl_xor(sum, o, 64);
+    const float mn = fmaxf(m, om);
+    sum = (m == -INFINITY ? 0.f : sum * expf(m - mn)) + (om == -INFINITY ? 0.f : os * expf(om - mn));
+    m = mn;
+  }
+  if ((threadIdx.x & 63) == 0) {
+    rm[threadIdx.x >> 6] = m;
+    rs[threadIdx.x >> 6] = sum;
+  }
+  __syncthreads();
+  float M = rm[0];
+  for (int w = 1; w < 4; ++w) M = fmaxf(M, rm[w]);
+  float Ssum = 0.f;
+  for (int w = 0; w < 4; ++w) Ssum += rs[w] * expf(rm[w] - M);
+  const float inv = 1.0f / Ssum;
+  const float scale = 1.0f / (float)n_rows;
+  const float zt = bf2f(z[row * ld + tgt]);
+  __syncthreads();
+  u32x4* dr = reinterpret_cast<u32x4*>(dz + row * ld);
+  for (int v = threadIdx.x; v < nv; v += blockDim.x) {
+    const u32x4 w = zr[v];
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float g[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int j = 8 * v + 2 * k + h;
+        const float x = __builtin_bit_cast(float, h ? (w[k] & 0xffff0000u) : (w[k] << 16));
+        g[h] = (j < V && valid) ? (expf(x - M) * inv - (j == tgt ? 1.0f : 0.0f)) * scale : 0.f;
+      }
+      o[k] = pack_bf2(g[0], g[1]);
+    }
+    dr[v] = o;
+  }
+  if (threadIdx.x == 0) loss_rows[row] = valid ? logf(Ssum) + M - zt : 0.0f;
 }
 
 __global__ void mean_kernel(const float* x, int64_t n, float* out) {
@@ -422,6 +561,7 @@ __global__ void mean_kernel(const float* x, int64_t n, float* out) {
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B, int T,
                              int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
                              hipStream_t s) {
+  if (ld % 8 || ld < V) return hipErrorInvalidValue;
   const int64_t rows = (int64_t)B * T;
   ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
   hipError_t e = hipGetLastError();

@@ -69,6 +69,8 @@ struct Gemm {
 // Validates shapes/alignment; returns a message or empty string.
 std::string gemm_check(const Gemm& g, bool f32_operands);
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t stream);
+// explicit tile configuration (0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 128x64)
+hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t stream);
 hipError_t launch_gemm_f32(const Gemm& g, hipStream_t stream);
 
 // ------------------------------------------------------------ glue kernels
@@ -76,10 +78,13 @@ hipError_t launch_embed_fwd(const int32_t* tokens, const float* wte, const float
                             int B, int T, int d, int V, hipStream_t s);
 hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int64_t rows, int d, hipStream_t s);
+// dg/db partial rows go to pg/pb (rows/16 x d each); cs_scratch holds
+// ceil(rows/16/128) x d floats for the final column sums.
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres,
-                                float* dx, float* dx_partial_g, float* dx_partial_b, float* dg,
+                                float* dx, float* pg, float* pb, float* cs_scratch, float* dg,
                                 float* db, int64_t rows, int d, hipStream_t s);
+// Column sums: partial must hold ceil(rows/128) x cols floats.
 hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
                               hipStream_t s);
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,

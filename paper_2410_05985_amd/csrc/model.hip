@@ -222,7 +222,7 @@ size_t carve(layup_ctx* c, char* base) {
     c->dqkv16 = cv.take<bf16_t>(N * 3 * d);
     c->ln_pg = cv.take<float>(cdiv(N, 16) * d);
     c->ln_pb = cv.take<float>(cdiv(N, 16) * d);
-    c->cs_part = cv.take<float>(cdiv(N, 256) * std::max<int64_t>(3 * d, F));
+    c->cs_part = cv.take<float>(cdiv(N, 128) * std::max<int64_t>(3 * d, F));
     c->splitk = cv.take<float>(SPLITK_BYTES / 4);
     c->splitk_bytes = SPLITK_BYTES;
   } else {
@@ -234,7 +234,7 @@ size_t carve(layup_ctx* c, char* base) {
     c->mlp_dz = cv.take<float>(g.batch * wmax);
     c->mlp_dh = cv.take<float>(g.batch * wmax);
     c->loss_rows = cv.take<float>(g.batch);
-    c->cs_part = cv.take<float>(cdiv(g.batch, 256) * wmax);
+    c->cs_part = cv.take<float>(cdiv(g.batch, 128) * wmax);
   }
   c->dis_partial = cv.take<float>(UM_MAX_BLOCKS);
   return cv.used + 256;
@@ -384,7 +384,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     TRY(run_gemm(c, dw, s, "head dW"));
     c->cur_dx = 0;
     HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
-                                   c->dx[0], c->ln_pg, c->ln_pb, fl.g("lnf.g"), fl.g("lnf.b"), N,
+                                   c->dx[0], c->ln_pg, c->ln_pb, c->cs_part, fl.g("lnf.g"), fl.g("lnf.b"), N,
                                    (int)d, s), "lnf backward");
     return LAYUP_OK;
   }
@@ -413,7 +413,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   TRY(run_gemm(c, mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32), s,
                "fc dX"));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
-                                 c->ln_pg, c->ln_pb, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
+                                 c->ln_pg, c->ln_pb, c->cs_part, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
   // attention output projection
   HIPCHK(c, launch_f32_to_bf16(c->dh, c->dy16, N * d, s), "dy2 cast");
@@ -456,7 +456,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   TRY(run_gemm(c, mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d,
                      EPI_F32), s, "qkv dX"));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
-                                 c->ln_pg, c->ln_pb, fl.g(p + "ln1.g"), fl.g(p + "ln1.b"), N, (int)d,
+                                 c->ln_pg, c->ln_pb, c->cs_part, fl.g(p + "ln1.g"), fl.g(p + "ln1.b"), N, (int)d,
                                  s), "ln1 backward");
   c->cur_dx ^= 1;
   return LAYUP_OK;

@@ -9,7 +9,8 @@
 // then the peer average  p2 = a*p1 + b*q  with a = 1-alpha, b = alpha, and
 // optionally the bfloat16 copy of p2 and the disagreement sum((p1-q)^2).
 //
-// Each tensor is read once and written once: 24 B/param for SGD momentum
+// Each tensor is read once and written once (streaming loads and stores):
+// 24 B/param for SGD momentum
 // (read p,g,m,q; write p,m), 32 B/param for AdamW (read p,g,m,v,q; write
 // p,m,v), +2 B with the bfloat16 copy.  Loads and stores are 128-bit; the
 // grid walks (tensor, chunk) pairs of a multi-tensor table so a layer of many
@@ -65,30 +66,45 @@ __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, 
     const float dfac = T.decay ? (1.0f - A.lr * A.wd) : 1.0f;
     const float wdc = T.decay ? A.wd : 0.0f;
     const int64_t vend = begin + ((end - begin) & ~(int64_t)3);
-    for (int64_t i = begin + 4 * threadIdx.x; i < vend; i += 4 * UM_THREADS) {
-      f32x4 p = *reinterpret_cast<const f32x4*>(T.p + i);
-      f32x4 g = *reinterpret_cast<const f32x4*>(T.g + i);
-      f32x4 m = *reinterpret_cast<const f32x4*>(T.m + i);
-      f32x4 q = *reinterpret_cast<const f32x4*>(T.q + i);
-      f32x4 v = {0.f, 0.f, 0.f, 0.f};
-      if (OPT == 1) v = *reinterpret_cast<const f32x4*>(T.v + i);
-      f32x4 po;
+    // two 4-element groups per thread per iteration, all loads issued before
+    // any math; streaming (nontemporal) loads and stores: every byte is used
+    // once, so nothing is kept in the caches
+    for (int64_t i0 = begin + 4 * threadIdx.x; i0 < vend; i0 += 8 * UM_THREADS) {
+      f32x4 p[2], g[2], m[2], v[2], q[2];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float pj = p[j], mj = m[j], vj = v[j], o;
-        um_elem<OPT>(pj, g[j], mj, vj, q[j], dfac, wdc, A, dis, o);
-        m[j] = mj;
-        v[j] = vj;
-        po[j] = o;
+      for (int u = 0; u < 2; ++u) {
+        const int64_t i = i0 + (int64_t)u * 4 * UM_THREADS;
+        if (i < vend) {
+          p[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.p + i));
+          g[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.g + i));
+          m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.m + i));
+          q[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.q + i));
+          v[u] = OPT == 1 ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.v + i))
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
       }
-      *reinterpret_cast<f32x4*>(T.p + i) = po;
-      *reinterpret_cast<f32x4*>(T.m + i) = m;
-      if (OPT == 1) *reinterpret_cast<f32x4*>(T.v + i) = v;
-      if (T.p16) {
-        u32x2 w;
-        w[0] = pack_bf2(po[0], po[1]);
-        w[1] = pack_bf2(po[2], po[3]);
-        *reinterpret_cast<u32x2*>(T.p16 + i) = w;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int64_t i = i0 + (int64_t)u * 4 * UM_THREADS;
+        if (i >= vend) continue;
+        f32x4 po;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float pj = p[u][j], mj = m[u][j], vj = v[u][j], o;
+          um_elem<OPT>(pj, g[u][j], mj, vj, q[u][j], dfac, wdc, A, dis, o);
+          m[u][j] = mj;
+          v[u][j] = vj;
+          po[j] = o;
+        }
+        __builtin_nontemporal_store(po, reinterpret_cast<f32x4*>(T.p + i));
+        __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(T.m + i));
+        if (OPT == 1) __builtin_nontemporal_store(v[u], reinterpret_cast<f32x4*>(T.v + i));
+        if (T.p16) {
+          u32x2 w;
+          w[0] = pack_bf2(po[0], po[1]);
+          w[1] = pack_bf2(po[2], po[3]);
+          __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(T.p16 + i));
+        }
       }
     }
     // ragged tail of the tensor (fewer than 4 elements)
