@@ -91,14 +91,15 @@ typedef short v8i16 __attribute__((ext_vector_type(8)));
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
 
 // Issue this wave's share of the direct-to-LDS copies of one ROWS x BKV tile.
-template <int ROWS, bool KMAJOR, int BKV>
+template <int ROWS, bool KMAJOR, int BKV, int NWAVES>
 __device__ __forceinline__ void issue_tile(const bf16_t* base, int64_t ld, int64_t r0, int64_t k0,
                                            int64_t R, int64_t K, char* lds, int wave, int lane) {
   constexpr int BLOCKS = ROWS * BKV * 2 / 1024;  // 1 KB blocks per tile
-  constexpr int PER_WAVE = BLOCKS / 4;
+  constexpr int PER_WAVE = (BLOCKS + NWAVES - 1) / NWAVES;
 #pragma unroll
   for (int i = 0; i < PER_WAVE; ++i) {
     const int blk = wave * PER_WAVE + i;
+    if (BLOCKS % NWAVES != 0 && blk >= BLOCKS) break;
     const bf16_t* src;
     if (KMAJOR) {
       constexpr int KCH = BKV / 8;           // 16-byte chunks per row
@@ -124,12 +125,12 @@ template <int ROWS, bool KMAJOR, int BKV>
 __device__ __forceinline__ void zero_tail(char* lds, int krem) {
   if (KMAJOR) {
     constexpr int KCH = BKV / 8;
-    for (int e = threadIdx.x; e < ROWS * KCH; e += THREADS) {
+    for (int e = threadIdx.x; e < ROWS * KCH; e += blockDim.x) {
       const int r = e / KCH, c = e % KCH;
       if (8 * c >= krem) *reinterpret_cast<u32x4*>(lds + km_off<BKV>(r, c)) = u32x4{0, 0, 0, 0};
     }
   } else {
-    for (int e = threadIdx.x; e < BKV * (ROWS / 8); e += THREADS) {
+    for (int e = threadIdx.x; e < BKV * (ROWS / 8); e += blockDim.x) {
       const int kk = e / (ROWS / 8), c = e % (ROWS / 8);
       if (kk >= krem) *reinterpret_cast<u32x4*>(lds + mm_off<ROWS>(kk, c)) = u32x4{0, 0, 0, 0};
     }
@@ -169,19 +170,21 @@ __device__ __forceinline__ void barrier_only() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN>
-struct TileCfg {
-  static constexpr int BKV = (BM * BN >= 256 * 256) ? 32 : 32;
-  static constexpr int STAGES = 4;
-};
-
-template <int BM, int BN, bool AK, bool BKM, int EPI, bool SPLIT>
-__global__ __launch_bounds__(THREADS, (BM * BN > 128 * 128) ? 1 : 2) void gemm_bf16_kernel(const KArgs P) {
-  constexpr int BKV = TileCfg<BM, BN>::BKV, STAGES = TileCfg<BM, BN>::STAGES;
-  constexpr int WM = BM / 2, WN = BN / 2;
+// WGM x WGN waves per workgroup; each wave owns a (BM/WGM) x (BN/WGN) block of
+// 32x32 MFMA tiles.  More waves issue more direct-to-LDS copies in parallel
+// (the copy rate per CU grows with the number of issuing waves).
+// STAGES LDS stages of (BM + BN) x 32 bf16; OCC workgroups per CU.
+template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool AK, bool BKM, int EPI, bool SPLIT>
+__global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KArgs P) {
+  constexpr int NW = WGM * WGN;
+  constexpr int BKV = 32;
+  constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int A_BYTES = BM * BKV * 2, STAGE = (BM + BN) * BKV * 2;
-  constexpr int LOADS = (BM + BN) * BKV * 2 / 1024 / 4;  // direct-to-LDS instructions per wave per K step
+  constexpr int A_BLK = BM * BKV * 2 / 1024, B_BLK = BN * BKV * 2 / 1024;
+  // direct-to-LDS instructions per wave per K step (same count on every wave)
+  constexpr int LOADS = (A_BLK + NW - 1) / NW + (B_BLK + NW - 1) / NW;
+  static_assert(A_BLK % NW == 0 && B_BLK % NW == 0, "copies must split evenly over the waves");
   constexpr int KS = BKV / 16;
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
@@ -210,7 +213,7 @@ __global__ __launch_bounds__(THREADS, (BM * BN > 128 * 128) ? 1 : 2) void gemm_b
   }
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -225,8 +228,8 @@ __global__ __launch_bounds__(THREADS, (BM * BN > 128 * 128) ? 1 : 2) void gemm_b
   auto issue = [&](int t) {
     char* st = smem + (t % STAGES) * STAGE;
     const int64_t k0 = kb + (int64_t)t * BKV;
-    issue_tile<BM, AK, BKV>(Ab, P.lda, m0, k0, P.M, ke, st, wave, lane);
-    issue_tile<BN, BKM, BKV>(Bb, P.ldb, n0, k0, P.N, ke, st + A_BYTES, wave, lane);
+    issue_tile<BM, AK, BKV, NW>(Ab, P.lda, m0, k0, P.M, ke, st, wave, lane);
+    issue_tile<BN, BKM, BKV, NW>(Bb, P.ldb, n0, k0, P.N, ke, st + A_BYTES, wave, lane);
   };
 #pragma unroll
   for (int t = 0; t < STAGES - 1; ++t)
@@ -340,12 +343,13 @@ __global__ void splitk_reduce_kernel(const KArgs P) {
   }
 }
 
-template <int BM, int BN, bool AK, bool BKM, int EPI>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI>
 hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   dim3 grid(P.tiles_m * P.tiles_n, P.splits > 1 ? P.splits : batch);
+  constexpr int NT = 64 * WGM * WGN;
   if constexpr (EPI == EPI_F32) {
     if (P.splits > 1) {
-      gemm_bf16_kernel<BM, BN, AK, BKM, EPI, true><<<grid, THREADS, 0, s>>>(P);
+      gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       int64_t total = P.M * P.N;
@@ -354,25 +358,25 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  gemm_bf16_kernel<BM, BN, AK, BKM, EPI, false><<<grid, THREADS, 0, s>>>(P);
+  gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, false><<<grid, NT, 0, s>>>(P);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int EPI>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, int EPI>
 hipError_t dispatch_layout(const Gemm& g, const KArgs& P, hipStream_t s) {
-  if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, true, true, EPI>(P, g.batch, s);
-  if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, true, false, EPI>(P, g.batch, s);
-  if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, false, false, EPI>(P, g.batch, s);
+  if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, true, EPI>(P, g.batch, s);
+  if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, false, EPI>(P, g.batch, s);
+  if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI>(P, g.batch, s);
   return hipErrorInvalidValue;  // m-major A with k-major B: no caller needs it
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC>
 hipError_t dispatch_epi(const Gemm& g, const KArgs& P, hipStream_t s) {
   switch (g.epi) {
-    case EPI_F32: return dispatch_layout<BM, BN, EPI_F32>(g, P, s);
-    case EPI_BF16: return dispatch_layout<BM, BN, EPI_BF16>(g, P, s);
-    case EPI_GELU: return dispatch_layout<BM, BN, EPI_GELU>(g, P, s);
-    default: return dispatch_layout<BM, BN, EPI_DGELU>(g, P, s);
+    case EPI_F32: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_F32>(g, P, s);
+    case EPI_BF16: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_BF16>(g, P, s);
+    case EPI_GELU: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_GELU>(g, P, s);
+    default: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_DGELU>(g, P, s);
   }
 }
 
@@ -404,31 +408,6 @@ KArgs make_args(const Gemm& g) {
 
 }  // namespace
 
-// Tile configurations: 0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 128x64.
-hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t s) {
-  if (g.M == 0 || g.N == 0) return hipSuccess;
-  static const int BMs[] = {256, 256, 128, 128, 128}, BNs[] = {256, 128, 256, 128, 64};
-  KArgs P = make_args(g);
-  const int BM = BMs[cfg], BN = BNs[cfg];
-  P.tiles_m = (int)cdiv(g.M, BM);
-  P.tiles_n = (int)cdiv(g.N, BN);
-  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32) {
-    while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
-    if (splits > 1) {
-      P.k_per_split = cdiv(cdiv(g.K, splits), BK) * BK;
-      P.splits = (int)cdiv(g.K, P.k_per_split);
-      P.partial = g.splitk_ws;
-    }
-  }
-  switch (cfg) {
-    case 0: return dispatch_epi<256, 256>(g, P, s);
-    case 1: return dispatch_epi<256, 128>(g, P, s);
-    case 2: return dispatch_epi<128, 256>(g, P, s);
-    case 3: return dispatch_epi<128, 128>(g, P, s);
-    default: return dispatch_epi<128, 64>(g, P, s);
-  }
-}
-
 std::string gemm_check(const Gemm& g, bool f32_operands) {
   if (g.M < 0 || g.N < 0 || g.K < 0) return "negative GEMM dimension";
   if (!f32_operands && !g.a_kmajor && g.b_kmajor) return "m-major A with k-major B is not supported";
@@ -441,38 +420,79 @@ std::string gemm_check(const Gemm& g, bool f32_operands) {
   if (g.lda < a_contig0 || g.ldb < b_contig0 || g.ldc < g.N) return "leading dimension smaller than the row";
   if (f32_operands) return "";  // scalar loads: no alignment rules
   const int64_t q = 8;
-  // contiguous dimension of each operand and all leading dims multiples of q
+  // contiguous dimension of each operand and all leading dims multiples of 8
   const int64_t a_contig = g.a_kmajor ? g.K : g.M;
   const int64_t b_contig = g.b_kmajor ? g.K : g.N;
-  if (a_contig % q || b_contig % q) return "contiguous GEMM dimensions must be multiples of 8 (bf16) / 4 (f32)";
-  if (g.lda % q || g.ldb % q) return "leading dimensions of A and B must be multiples of 8 (bf16) / 4 (f32)";
+  if (a_contig % q || b_contig % q) return "contiguous GEMM dimensions must be multiples of 8 (bf16)";
+  if (g.lda % q || g.ldb % q) return "leading dimensions of A and B must be multiples of 8 (bf16)";
   if (((uintptr_t)g.A | (uintptr_t)g.B) & 15) return "A and B must be 16-byte aligned";
   if ((g.a_outer | g.a_inner | g.b_outer | g.b_inner) % q) return "batch strides must keep 16-byte alignment";
   return "";
 }
 
-// Tile choice (measured on MI355X): 256x256 pays off only when both output
-// dimensions and K are large; otherwise 128x128 (two workgroups per CU) is
-// faster.  N <= 64 (attention head width) takes 128x64.  Split-K when the
-// output has fewer tiles than CUs and K is long (the dW GEMMs).
+// Tile configurations: tile, wave grid, LDS stages, workgroups per CU.  The
+// copy rate into LDS grows with the number of waves issuing direct-to-LDS
+// loads, so the configurations trade tile size (operand reuse) against waves
+// per CU.
+struct TileShape { int bm, bn; };
+static const TileShape kShapes[] = {
+    {256, 256},  // 0: 4x2 waves (each 64x128), 4 stages, 1/CU  (8 waves/CU)
+    {128, 128},  // 1: 2x4 waves (each 64x32),  3 stages, 3/CU  (24 waves/CU)
+    {128, 64},   // 2: 2x2 waves (each 64x32),  4 stages, 3/CU  (12 waves/CU)
+    {128, 128},  // 3: 2x2 waves (each 64x64),  4 stages, 2/CU  (8 waves/CU)
+};
+constexpr int kNumCfg = 4;
+
+hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  if (cfg < 0 || cfg >= kNumCfg) return hipErrorInvalidValue;
+  KArgs P = make_args(g);
+  const int BM = kShapes[cfg].bm, BN = kShapes[cfg].bn;
+  P.tiles_m = (int)cdiv(g.M, BM);
+  P.tiles_n = (int)cdiv(g.N, BN);
+  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32) {
+    while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
+    if (splits > 1) {
+      P.k_per_split = cdiv(cdiv(g.K, splits), 32) * 32;
+      P.splits = (int)cdiv(g.K, P.k_per_split);
+      P.partial = g.splitk_ws;
+    }
+  }
+  switch (cfg) {
+    case 0: return dispatch_epi<256, 256, 4, 2, 4, 1>(g, P, s);
+    case 1: return dispatch_epi<128, 128, 2, 4, 3, 3>(g, P, s);
+    case 2: return dispatch_epi<128, 64, 2, 2, 4, 3>(g, P, s);
+    default: return dispatch_epi<128, 128, 2, 2, 4, 2>(g, P, s);
+  }
+}
+
+// Tile choice (measured on MI355X over the GPT-2-small/medium/1.3B shapes):
+// 256x256 with 8 waves when both output dimensions and K are large; the
+// 8-wave 128x128 tile elsewhere; 128x64 when N <= 64 (attention head width).
+// Split-K (float32 partials, fixed-order sum) when K >= 1536 and the output
+// has too few tiles to occupy every CU (fewer than 256 tiles of 256x256, or
+// 512 of 128x128).
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
-  const int64_t cus = 256;
   auto tiles = [&](int bm, int bn) { return cdiv(g.M, bm) * cdiv(g.N, bn) * g.batch; };
-  int cfg, bm = 128, bn = 128;
+  int cfg;
+  int64_t t;
   if (g.N <= 64) {
-    cfg = 4;
-    bn = 64;
-  } else if (tiles(256, 256) >= cus && g.K >= 4096) {
+    cfg = 2;
+    t = tiles(128, 64);
+  } else if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256) {
     cfg = 0;
-    bm = bn = 256;
+    t = tiles(256, 256);
   } else {
-    cfg = 3;
+    cfg = 1;
+    t = tiles(128, 128);
   }
+  // workgroups that keep every CU busy: one 256x256 tile or three 128x128
+  // tiles per CU at a time
+  const int64_t want = cfg == 0 ? 256 : 512;
   int splits = 1;
-  const int64_t t = tiles(bm, bn);
-  if (g.batch == 1 && t < cus && g.K >= 1024)
-    splits = (int)std::min<int64_t>(std::max<int64_t>(1, (2 * cus) / t), g.K / 512);
+  if (g.batch == 1 && t < want && g.K >= 1536)
+    splits = (int)std::min<int64_t>(std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), g.K / 512), 8);
   return launch_gemm_bf16_cfg(g, cfg, splits, s);
 }
 
