@@ -13,7 +13,16 @@ Prints ONE JSON line.  ``value`` is ms per layer-wise step (lower is better);
 the per-kernel figures (update+mix HBM GB/s, backward-GEMM TFLOP/s) are
 measured with HIP events on the stream the kernels run on.
 
+Other workloads (one JSON line each, not the default bench line):
+  --workload gpt2-medium   24 x 1024, 16 heads, MLP 4096, T 1024, batch 8
+  --workload gpt-1.3b      24 x 2048, 16 heads, MLP 8192, T 2048, batch 4, 3
+                           resident peer replicas, peer slot drawn per step
+  --workload resnet50-update  update+mix sweep over the 161 ResNet-50
+                           tensors (54 units in reverse order), SGD momentum
+  --workload mlp           tiny float32 MLP, 10 layer-wise steps
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                       [--workload NAME]
 """
 from __future__ import annotations
 
@@ -41,6 +50,8 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
+    ap.add_argument("--workload", default="gpt2-small",
+                    choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp"])
     return ap.parse_args()
 
 
@@ -145,6 +156,176 @@ def cpu_baseline(cfg_full):
                        f"({dt:.1f} s), scaled by GEMM FLOPs x{scale:.2f} to 12 blocks x batch 8")
 
 
+def gpt_model_on_device(torch, LU, S, cfg, n_peers):
+    """Model buffers filled on the device from seeded torch generators (the
+    1.3B stack would take minutes to draw on the host): matrices and
+    embeddings N(0, 0.02), biases 0, LayerNorm gain 1; peer replica k = own +
+    N(0, 1e-3) from seed 2 + 100 k.  Embedding padding rows stay zero."""
+    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch, cfg.vocab,
+                       n_peers)
+    model = LU.Model(lc, "adamw")
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(1)
+    for t in model.infos:
+        view = model.params[t["offset"]: t["offset"] + t["numel"]]
+        if t["cols"] > 1:
+            view.normal_(0.0, 0.02, generator=gen)
+        elif t["name"].endswith(".g"):
+            view.fill_(1.0)
+    for k in range(n_peers):
+        gen.manual_seed(2 + 100 * k)
+        peer = model.peers[k * model.total: (k + 1) * model.total]
+        peer.copy_(model.params)
+        noise = torch.empty_like(peer).normal_(0.0, 1e-3, generator=gen)
+        for t in model.infos:   # logical elements only
+            o = t["offset"]
+            peer[o: o + t["numel"]] += noise[o: o + t["numel"]]
+        del noise
+    torch.cuda.synchronize()
+    LU.layup_refresh_shadow(model.ctx)
+    model.synchronize()
+    return model
+
+
+def bench_gpt_other(args, torch, LU, S, name):
+    cfg = S.GPT2_MEDIUM if name == "gpt2-medium" else S.GPT_1P3B
+    model = gpt_model_on_device(torch, LU, S, cfg, cfg.n_peers)
+    tokens = torch.from_numpy(S.gpt_tokens(cfg)).to("cuda")
+    slots = S.peer_slots(args.warmup + args.steps, cfg.n_peers)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, 1)
+    step = 0
+    for _ in range(args.warmup):
+        hp.step = step + 1
+        LU.layup_step(model.ctx, tokens, None, hp, cfg.alpha, int(slots[step]), loss)
+        step += 1
+    model.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        hp.step = step + 1
+        LU.layup_step(model.ctx, tokens, None, hp, cfg.alpha, int(slots[step]), loss)
+        step += 1
+    model.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    ks = torch.cuda.Stream()
+    blk, head = backward_gemm_shapes(cfg)
+    g = time_gemms(torch, LU, blk, args.kernel_reps, ks)
+    blk_ms = sum(x["ms"] for x in g)
+    blk_flops = sum(2.0 * x["M"] * x["N"] * x["K"] for x in g)
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    um = time_update_mix(torch, LU, model, 1, hp, cfg.alpha, args.kernel_reps, ks, flush)
+    out = {"metric": "ms per layer-wise step", "value": round(ms, 3), "unit": "ms/step",
+           "workload": name, "n_params": cfg.n_params(), "steps": args.steps, "warmup": args.warmup,
+           "tokens_per_s": round(cfg.batch * cfg.seq / (ms * 1e-3), 1), "loss": round(float(loss.item()), 5),
+           "backward_gemm_TFLOPs": round(blk_flops / (blk_ms * 1e-3) / 1e12, 2),
+           "backward_gemm_frac": round(blk_flops / (blk_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "update_mix_GBps": round(um["gbs"], 1), "update_mix_frac_hbm": round(um["gbs"] / PEAK_HBM_GBS, 4),
+           "update_mix_unit_bytes": um["bytes"], "data": "synthetic (device-seeded)",
+           "peer_slots": "seed 3, uniform over %d resident replicas" % cfg.n_peers}
+    model.close()
+    print(json.dumps(out), flush=True)
+
+
+def bench_resnet(args, torch, LU, S):
+    """Update+mix sweep over the 161 ResNet-50 tensors, 54 units in reverse
+    order, SGD momentum 0.9, wd 5e-5 on every tensor, lr 0.1, alpha 0.5;
+    24 B/param (read p, g, m, q; write p, m).  Reported three ways: the
+    kernel-time-weighted rate of the per-unit launches, the wall-clock rate of
+    the sweep (launch gaps included) and one launch sequence covering all 161
+    tensors (16 per launch)."""
+    params, grads, peer = S.resnet50_tensors()
+    specs = S.resnet50_param_specs()
+    units = S.resnet50_units()
+    off, o = {}, 0
+    for n, shp, _ in specs:
+        off[n] = o
+        o += (int(np.prod(shp)) + 63) // 64 * 64
+    total = o
+    bufs = {k: torch.zeros(total, dtype=torch.float32, device="cuda") for k in ("p", "g", "m", "q")}
+    for name, arr in (("p", params), ("g", grads), ("q", peer)):
+        host = torch.zeros(total, dtype=torch.float32)
+        for n, a in arr.items():
+            host[off[n]: off[n] + a.size] = torch.from_numpy(a.reshape(-1))
+        bufs[name].copy_(host.cuda())
+    def desc(n):
+        k = off[n]
+        return LU.layup_tensor(param=bufs["p"].data_ptr() + 4 * k, grad=bufs["g"].data_ptr() + 4 * k,
+                               state0=bufs["m"].data_ptr() + 4 * k, state1=None,
+                               peer=bufs["q"].data_ptr() + 4 * k, param_bf16=None,
+                               numel=int(params[n].size), decay=1)
+    unit_descs = [[desc(n) for n in u] for u in units]
+    all_descs = [desc(n) for n, _, _ in specs]
+    n_params = sum(a.size for a in params.values())
+    hp = LU.hparams("sgd", 0.1, 0.9, 5e-5)
+    st = torch.cuda.Stream()
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    # per-unit kernel times
+    kern_ms, wall_ms, single_ms = 0.0, 0.0, 0.0
+    reps = max(1, args.kernel_reps // 4)
+    with torch.cuda.stream(st):
+        for r in range(reps + 1):
+            flush.add_(1.0)
+            evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(units))]
+            w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            w0.record(st)
+            for i, u in enumerate(reversed(range(len(units)))):
+                evs[2 * i].record(st)
+                LU.layup_layer_update_mix(None, unit_descs[u], hp, 0.5, stream=st)
+                evs[2 * i + 1].record(st)
+            w1.record(st)
+            w1.synchronize()
+            if r > 0:
+                kern_ms += sum(evs[2 * i].elapsed_time(evs[2 * i + 1]) for i in range(len(units)))
+                wall_ms += w0.elapsed_time(w1)
+        for r in range(reps + 1):
+            flush.add_(1.0)
+            w0, w1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            w0.record(st)
+            LU.layup_layer_update_mix(None, all_descs, hp, 0.5, stream=st)
+            w1.record(st)
+            w1.synchronize()
+            if r > 0:
+                single_ms += w0.elapsed_time(w1)
+    nbytes = 24 * n_params
+    kern_ms, wall_ms, single_ms = kern_ms / reps, wall_ms / reps, single_ms / reps
+    out = {"metric": "update+mix HBM GB/s (ResNet-50 parameter set, layer-wise sweep)",
+           "workload": "resnet50-update", "value": round(nbytes / (kern_ms * 1e-3) / 1e9, 1), "unit": "GB/s",
+           "n_tensors": len(specs), "n_units": len(units), "n_params": int(n_params), "bytes": nbytes,
+           "kernel_weighted_GBps": round(nbytes / (kern_ms * 1e-3) / 1e9, 1),
+           "sweep_wall_GBps": round(nbytes / (wall_ms * 1e-3) / 1e9, 1),
+           "all_tensors_GBps": round(nbytes / (single_ms * 1e-3) / 1e9, 1),
+           "sweep_kernel_ms": round(kern_ms, 4), "sweep_wall_ms": round(wall_ms, 4),
+           "frac_hbm": round(nbytes / (kern_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4), "data": "synthetic"}
+    print(json.dumps(out), flush=True)
+
+
+def bench_mlp(args, torch, LU, S):
+    cfg = S.MLP_TINY
+    x, y = S.mlp_inputs(cfg)
+    m = LU.Model(LU.mlp_config(cfg.dims, cfg.batch), "sgd")
+    m.load("params", S.mlp_params(cfg))
+    m.load("peers", S.peer_of(S.mlp_params(cfg), 0.01))
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    hp = LU.hparams("sgd", cfg.lr, cfg.momentum, 0.0)
+    torch.cuda.synchronize()
+    for s_ in range(cfg.steps):
+        LU.layup_step(m.ctx, yd[s_], xd[s_], hp, cfg.alpha, 0)
+    m.synchronize()
+    reps = 20
+    t0 = time.perf_counter()
+    for r in range(reps):
+        for s_ in range(cfg.steps):
+            LU.layup_step(m.ctx, yd[s_], xd[s_], hp, cfg.alpha, 0)
+    m.synchronize()
+    us = (time.perf_counter() - t0) * 1e6 / (reps * cfg.steps)
+    print(json.dumps({"metric": "us per layer-wise step (tiny MLP, float32)", "workload": "mlp",
+                      "value": round(us, 2), "unit": "us/step", "steps": reps * cfg.steps,
+                      "note": "launch-latency bound: 3 units, 4.8 MB of update+mix and ~30 MFLOP per step"}),
+          flush=True)
+    m.close()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -152,6 +333,16 @@ def main():
                                    "multi-GPU runs are not part of it", "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
+    if args.workload != "gpt2-small":
+        from paper_2410_05985_amd import layup as LU
+        from paper_2410_05985_amd import synthetic as S
+        if args.workload == "resnet50-update":
+            bench_resnet(args, torch, LU, S)
+        elif args.workload == "mlp":
+            bench_mlp(args, torch, LU, S)
+        else:
+            bench_gpt_other(args, torch, LU, S, args.workload)
+        return
     from paper_2410_05985_amd import layup as LU
     from paper_2410_05985_amd import synthetic as S
 

@@ -40,6 +40,7 @@ struct KArgs {
   int64_t M, N, K, lda, ldb, ldc;
   int64_t a_outer, a_inner, b_outer, b_inner, c_outer, c_inner;
   int32_t inner, splits, tiles_m, tiles_n;
+  int32_t causal, pad_;
   int64_t k_per_split;
 };
 
@@ -211,6 +212,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
     kb = split * P.k_per_split;
     ke = min(P.K, kb + P.k_per_split);
   }
+  if (P.causal == CAUSAL_OUT_LOWER && n0 > m0 + BM - 1) return;  // whole tile above the diagonal
+  if (P.causal == CAUSAL_A_LOWER) ke = min(ke, m0 + BM);
+  if (P.causal == CAUSAL_A_UPPER) kb = max(kb, m0);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -403,6 +407,7 @@ KArgs make_args(const Gemm& g) {
   P.c_inner = g.c_inner;
   P.inner = g.inner;
   P.splits = 1;
+  P.causal = g.causal;
   return P;
 }
 

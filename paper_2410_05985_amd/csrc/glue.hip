@@ -333,12 +333,19 @@ __global__ void colsum_scalar(const T* x, int64_t rows, int64_t cols, int64_t ld
   partial[(int64_t)blockIdx.y * cols + c] = s;
 }
 
-__global__ void colsum_final_kernel(const float* partial, int64_t chunks, int64_t cols, float* out) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= cols) return;
+// 64 columns x 4 chunk lanes per block: lane l sums chunks l, l+4, ... in
+// order, then the four lane sums are added in lane order.
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial, int64_t chunks,
+                                                           int64_t cols, float* out) {
+  __shared__ float red[4][64];
+  const int cl = threadIdx.x & 63, l = threadIdx.x >> 6;
+  const int64_t c = (int64_t)blockIdx.x * 64 + cl;
   float s = 0.f;
-  for (int64_t k = 0; k < chunks; ++k) s += partial[k * cols + c];
-  out[c] = s;
+  if (c < cols)
+    for (int64_t k = l; k < chunks; k += 4) s += partial[k * cols + c];
+  red[l][cl] = s;
+  __syncthreads();
+  if (l == 0 && c < cols) out[c] = (red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl]);
 }
 
 template <typename T>
@@ -356,7 +363,7 @@ hipError_t colsum(const T* x, int64_t rows, int64_t cols, int64_t ld, float* par
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  colsum_final_kernel<<<(unsigned)cdiv(cols, 256), 256, 0, s>>>(partial, chunks, cols, out);
+  colsum_final_kernel<<<(unsigned)cdiv(cols, 64), 256, 0, s>>>(partial, chunks, cols, out);
   return hipGetLastError();
 }
 

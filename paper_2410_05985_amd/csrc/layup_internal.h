@@ -64,7 +64,14 @@ struct Gemm {
   int64_t a_outer = 0, a_inner = 0, b_outer = 0, b_inner = 0, c_outer = 0, c_inner = 0;
   float* splitk_ws = nullptr;  // float32 partials for split-K (batch 1 only)
   size_t splitk_ws_bytes = 0;
+  // Causal structure of square attention products (M = N or M = K = T):
+  //   CAUSAL_OUT_LOWER: only outputs with n <= m are needed (S, dP); tiles
+  //     strictly above the diagonal are skipped and left unwritten.
+  //   CAUSAL_A_LOWER: A(m, k) = 0 for k > m (P V, dS K): K stops at the tile's last row.
+  //   CAUSAL_A_UPPER: A(m, k) = 0 for k < m (P^T dO, dS^T Q): K starts at the tile's first row.
+  int causal = 0;
 };
+enum Causal : int { CAUSAL_NONE = 0, CAUSAL_OUT_LOWER = 1, CAUSAL_A_LOWER = 2, CAUSAL_A_UPPER = 3 };
 
 // Validates shapes/alignment; returns a message or empty string.
 std::string gemm_check(const Gemm& g, bool f32_operands);

@@ -332,6 +332,7 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
     sg.a_inner = sg.b_inner = dh;
     sg.c_outer = H * T * T;
     sg.c_inner = T * T;
+    sg.causal = CAUSAL_OUT_LOWER;
     TRY(run_gemm(c, sg, s, "scores"));
     HIPCHK(c, launch_softmax_fwd(c->S, A.P, B * H, (int)T, scale, s), "softmax");
     // o_h = P V_h
@@ -344,6 +345,7 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
     pv.b_inner = dh;
     pv.c_outer = T * d;
     pv.c_inner = dh;
+    pv.causal = CAUSAL_A_LOWER;
     TRY(run_gemm(c, pv, s, "attention output"));
     Gemm pr = mk(true, true, N, d, d, A.o, d, fl.w16(p + "proj.w"), d, A.h, d, EPI_F32);
     pr.bias = fl.p(p + "proj.b");
@@ -424,7 +426,8 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                s, "proj dX"));
   // attention core, batched over z = b*H + h
   auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
-                     int64_t ci) {
+                     int64_t ci, int causal) {
+    gm.causal = causal;
     gm.batch = (int)(B * H);
     gm.inner = (int)H;
     gm.a_outer = ao;
@@ -438,17 +441,17 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   const int64_t TT = T * T;
   // dP = dO_h V_h^T
   TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
-                          T * d, dh, T * 3 * d, dh, H * TT, TT), s, "dP"));
+                          T * d, dh, T * 3 * d, dh, H * TT, TT, CAUSAL_OUT_LOWER), s, "dP"));
   // dV_h = P^T dO_h
   TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
-                             EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh), s, "dV"));
+                             EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dV"));
   HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
   // dQ_h = dS K_h
   TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
-                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh), s, "dQ"));
+                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_LOWER), s, "dQ"));
   // dK_h = dS^T Q_h
   TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
-                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh), s, "dK"));
+                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   // qkv projection
   TRY(run_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
                      EPI_F32), s, "qkv dW"));
