@@ -20,6 +20,9 @@ Other workloads (one JSON line each, not the default bench line):
   --workload resnet50-update  update+mix sweep over the 161 ResNet-50
                            tensors (54 units in reverse order), SGD momentum
   --workload mlp           tiny float32 MLP, 10 layer-wise steps
+  --workload kernels       one launch each of: a 1 GiB copy (counter
+                           calibration), one GPT-2-small block's 8 backward
+                           GEMMs, one block's update+mix -- for rocprofv3 --pmc
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                        [--workload NAME]
@@ -38,6 +41,8 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+import hashlib
+
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, GB/s
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, TFLOP/s
 
@@ -51,8 +56,24 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
     ap.add_argument("--workload", default="gpt2-small",
-                    choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp"])
+                    choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp",
+                             "kernels"])
     return ap.parse_args()
+
+
+def measured_traffic(key, source):
+    """HBM bytes per launch sequence from the committed counter summary
+    (profiles/pmc_traffic.json: FETCH_SIZE + WRITE_SIZE, copy-calibrated),
+    or None when the kernel source has changed since the counters were
+    taken."""
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "pmc_traffic.json")))[key]
+        sha = hashlib.sha256(open(os.path.join(ROOT, "paper_2410_05985_amd", "csrc", source), "rb").read())
+        if sha.hexdigest()[:16] != rec["source_sha256_16"]:
+            return None
+        return rec["hbm_bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def backward_gemm_shapes(cfg):
@@ -91,36 +112,42 @@ def time_gemms(torch, LU, shapes, reps, stream):
     return res
 
 
-def time_update_mix(torch, LU, m, unit, hp, alpha, reps, stream, flush):
+def time_update_mix(torch, LU, m, units, hp, alpha, reps, stream):
     """Average duration of one unit's update+mix launch (AdamW + bf16 copy)
-    with HIP events on the update stream; the 512 MB flush buffer is
-    rewritten between launches so the unit's 241 MB are not served from the
-    256 MB MALL."""
-    t = [x for x in m.infos if x["unit"] == unit]
-    numel = sum(x["numel"] for x in t)
+    with HIP events on the update stream.  The units are launched back to
+    back, one launch per unit, as in the step; the round over all block units
+    (12 x 241 MB for GPT-2-small) is far larger than the 256 MB MALL, so no
+    launch finds its operands in the cache."""
     descs = []
-    for x in t:
-        o = x["offset"]
-        descs.append(LU.layup_tensor(param=m.params.data_ptr() + 4 * o, grad=m.grads.data_ptr() + 4 * o,
+    numel = None
+    for unit in units:
+        t = [x for x in m.infos if x["unit"] == unit]
+        n = sum(x["numel"] for x in t)
+        assert numel is None or n == numel, "units of equal size"
+        numel = n
+        d = []
+        for x in t:
+            o = x["offset"]
+            d.append(LU.layup_tensor(param=m.params.data_ptr() + 4 * o, grad=m.grads.data_ptr() + 4 * o,
                                      state0=m.m.data_ptr() + 4 * o, state1=m.v.data_ptr() + 4 * o,
                                      peer=m.peers.data_ptr() + 4 * o,
                                      param_bf16=m.params_bf16.data_ptr() + 2 * o,
                                      numel=x["numel"], decay=x["decay"]))
-    ms_tot = 0.0
+        descs.append(d)
     hp.step = 1
     with torch.cuda.stream(stream):
-        for r in range(reps + 2):
-            flush.add_(1.0)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            LU.layup_layer_update_mix(None, descs, hp, alpha, stream=stream)
-            e1.record(stream)
-            e1.synchronize()
-            if r >= 2:
-                ms_tot += e0.elapsed_time(e1)
-    ms = ms_tot / reps
+        for d in descs:
+            LU.layup_layer_update_mix(None, d, hp, alpha, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            for d in descs:
+                LU.layup_layer_update_mix(None, d, hp, alpha, stream=stream)
+        e1.record(stream)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / (reps * len(descs))
     nbytes = 34 * numel   # AdamW 32 B/param + 2 B bf16 copy
-    return dict(unit=unit, numel=numel, ms=ms, bytes=nbytes, gbs=nbytes / (ms * 1e-3) / 1e9)
+    return dict(units=len(descs), numel=numel, ms=ms, bytes=nbytes, gbs=nbytes / (ms * 1e-3) / 1e9)
 
 
 def cpu_baseline(cfg_full):
@@ -212,8 +239,7 @@ def bench_gpt_other(args, torch, LU, S, name):
     g = time_gemms(torch, LU, blk, args.kernel_reps, ks)
     blk_ms = sum(x["ms"] for x in g)
     blk_flops = sum(2.0 * x["M"] * x["N"] * x["K"] for x in g)
-    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
-    um = time_update_mix(torch, LU, model, 1, hp, cfg.alpha, args.kernel_reps, ks, flush)
+    um = time_update_mix(torch, LU, model, range(1, cfg.n_layer + 1), hp, cfg.alpha, args.kernel_reps, ks)
     out = {"metric": "ms per layer-wise step", "value": round(ms, 3), "unit": "ms/step",
            "workload": name, "n_params": cfg.n_params(), "steps": args.steps, "warmup": args.warmup,
            "tokens_per_s": round(cfg.batch * cfg.seq / (ms * 1e-3), 1), "loss": round(float(loss.item()), 5),
@@ -326,6 +352,48 @@ def bench_mlp(args, torch, LU, S):
     m.close()
 
 
+def bench_kernels(args, torch, LU, S):
+    """Single launches for hardware-counter runs, in this order: a 1 GiB
+    device copy (known traffic: 1 GiB read + 1 GiB written), the 8 backward
+    GEMMs of one GPT-2-small block (qkv, proj, fc, mproj; dX then dW), the
+    update+mix of one GPT-2-small block (AdamW + bf16 copy).  The device is
+    synchronised between launches so each dispatch stands alone."""
+    cfg = S.GPT2_SMALL
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    blk, _ = backward_gemm_shapes(cfg)
+    ops = []
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+    for name, M, N, K, ak, bk in blk:
+        A = torch.randn((M, K) if ak else (K, M), device="cuda").to(torch.bfloat16)
+        B = torch.randn((N, K) if bk else (K, N), device="cuda").to(torch.bfloat16)
+        C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        ops.append((name, LU.gemm_desc(A, B, C, M, N, K, K if ak else M, K if bk else N, N, ak, bk, True,
+                                       workspace=ws, workspace_bytes=64 << 20), (A, B, C)))
+    n = 7_087_872
+    bufs = [torch.randn(n, device="cuda") * 1e-3 for _ in range(5)]
+    p16 = torch.zeros(n, dtype=torch.int16, device="cuda")
+    bufs[3].abs_()
+    t = LU.layup_tensor(param=bufs[0].data_ptr(), grad=bufs[1].data_ptr(), state0=bufs[2].data_ptr(),
+                        state1=bufs[3].data_ptr(), peer=bufs[4].data_ptr(), param_bf16=p16.data_ptr(),
+                        numel=n, decay=1)
+    hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, 1)
+    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    for name, d, _ in ops:
+        LU.layup_gemm_bf16(d, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+    flush.add_(1.0)
+    torch.cuda.synchronize()
+    LU.layup_layer_update_mix(None, [t], hp, cfg.alpha, stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    print(json.dumps({"workload": "kernels", "copy_bytes": 2 * src.numel() * 4,
+                      "gemms": [o[0] for o in ops], "update_mix_numel": n,
+                      "update_mix_algorithmic_bytes": 34 * n}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -338,6 +406,8 @@ def main():
         from paper_2410_05985_amd import synthetic as S
         if args.workload == "resnet50-update":
             bench_resnet(args, torch, LU, S)
+        elif args.workload == "kernels":
+            bench_kernels(args, torch, LU, S)
         elif args.workload == "mlp":
             bench_mlp(args, torch, LU, S)
         else:
@@ -386,8 +456,7 @@ def main():
     blk_ms = sum(x["ms"] for x in g[:len(blk)])
     blk_flops = sum(2.0 * x["M"] * x["N"] * x["K"] for x in g[:len(blk)])
     gemm_tflops = blk_flops / (blk_ms * 1e-3) / 1e12
-    flush = torch.empty(128 << 20, dtype=torch.float32, device="cuda")
-    um = time_update_mix(torch, LU, model, 1, hp, cfg.alpha, args.kernel_reps, ks, flush)
+    um = time_update_mix(torch, LU, model, range(1, cfg.n_layer + 1), hp, cfg.alpha, args.kernel_reps, ks)
     for x in g:
         print(f"[bench] gemm {x['name']:9s} {x['M']}x{x['N']}x{x['K']}: {x['ms']*1e3:8.1f} us "
               f"{x['tflops']:7.1f} TFLOP/s", file=sys.stderr, flush=True)
@@ -395,10 +464,13 @@ def main():
           file=sys.stderr, flush=True)
 
     # dominant kernel of the step: the backward GEMMs of a block (MFMA bound)
+    traffic = measured_traffic("gemm_block_backward", "gemm_bf16.hip")
     roofline = dict(bound="mfma", achieved=round(gemm_tflops, 2), peak=PEAK_BF16_TFLOPS,
-                    unit="TFLOP/s", frac=round(gemm_tflops / PEAK_BF16_TFLOPS, 4), traffic=None,
-                    kernel="gemm_bf16_kernel (one block's 8 backward dX/dW GEMMs)",
-                    algorithmic_flops_per_block=blk_flops)
+                    unit="TFLOP/s", frac=round(gemm_tflops / PEAK_BF16_TFLOPS, 4),
+                    traffic=traffic,
+                    kernel="gemm_bf16_kernel (one block's 8 backward dX/dW GEMMs + split-K sums)",
+                    algorithmic_flops_per_block=blk_flops,
+                    launch_ms_per_block=round(blk_ms, 5))
     out = {
         "metric": "update+mix HBM GB/s; backward GEMM TFLOPS; ms per layer-wise step (GPT-2-small)",
         "value": round(ms_step, 4),
@@ -419,6 +491,10 @@ def main():
         "tokens_per_s": round(cfg.batch * cfg.seq / (ms_step * 1e-3), 1),
         "update_mix_GBps": round(um["gbs"], 1),
         "update_mix_frac_hbm": round(um["gbs"] / PEAK_HBM_GBS, 4),
+        "update_mix_roofline": {"bound": "hbm", "achieved": round(um["gbs"], 1), "peak": PEAK_HBM_GBS,
+                                "unit": "GB/s", "frac": round(um["gbs"] / PEAK_HBM_GBS, 4),
+                                "traffic": measured_traffic("update_mix_block", "update_mix.hip"),
+                                "algorithmic_bytes": um["bytes"]},
         "backward_gemm_TFLOPs": round(gemm_tflops, 2),
         "head_gemm_TFLOPs": [round(x["tflops"], 1) for x in g[len(blk):]],
         "loss": round(loss_v, 5),

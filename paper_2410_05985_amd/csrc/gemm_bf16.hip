@@ -40,7 +40,7 @@ struct KArgs {
   int64_t M, N, K, lda, ldb, ldc;
   int64_t a_outer, a_inner, b_outer, b_inner, c_outer, c_inner;
   int32_t inner, splits, tiles_m, tiles_n;
-  int32_t causal, pad_;
+  int32_t causal, nz;      // nz: batch count
   int64_t k_per_split;
 };
 
@@ -189,10 +189,18 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   constexpr int KS = BKV / 16;
   __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
-  // ---- tile mapping: XCD-aware remap, then group along M
+  // ---- tile mapping.  The grid is one dimension of (batch or split) x
+  // tiles, padded to a multiple of 8.  Workgroups are dealt round-robin over
+  // the 8 XCDs (each with its own L2), so hardware id h runs on XCD h % 8:
+  // the remap gives every XCD a contiguous range of logical ids, i.e. whole
+  // bands of tiles of one batch/split that share operand rows.  Inside a
+  // batch/split, tiles go in groups of 8 tile-rows for L2 reuse of B.
   const int n_tiles = P.tiles_m * P.tiles_n;
-  int id = blockIdx.x;
-  if ((n_tiles & 7) == 0) id = (id & 7) * (n_tiles >> 3) + (id >> 3);
+  const int n_log = n_tiles * (SPLIT ? P.splits : P.nz);
+  const int h = blockIdx.x;
+  const int lid = (h & 7) * (int)(gridDim.x >> 3) + (h >> 3);
+  if (lid >= n_log) return;
+  const int zz = lid / n_tiles, id = lid % n_tiles;
   constexpr int GROUP = 8;
   const int width = GROUP * P.tiles_n;
   const int grp = id / width;
@@ -201,8 +209,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   const int tm = first_m + (id % width) % gsz;
   const int tn = (id % width) / gsz;
 
-  const int z = SPLIT ? 0 : blockIdx.y;
-  const int split = SPLIT ? blockIdx.y : 0;
+  const int z = SPLIT ? 0 : zz;
+  const int split = SPLIT ? zz : 0;
   const int zo = z / P.inner, zi = z % P.inner;
   const bf16_t* Ab = P.A + zo * P.a_outer + zi * P.a_inner;
   const bf16_t* Bb = P.B + zo * P.b_outer + zi * P.b_inner;
@@ -349,7 +357,9 @@ __global__ void splitk_reduce_kernel(const KArgs P) {
 
 template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI>
 hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
-  dim3 grid(P.tiles_m * P.tiles_n, P.splits > 1 ? P.splits : batch);
+  const int64_t n_log = (int64_t)P.tiles_m * P.tiles_n * (P.splits > 1 ? P.splits : batch);
+  if (n_log >= (1ll << 31) - 8) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((n_log + 7) / 8 * 8));
   constexpr int NT = 64 * WGM * WGN;
   if constexpr (EPI == EPI_F32) {
     if (P.splits > 1) {
@@ -408,6 +418,7 @@ KArgs make_args(const Gemm& g) {
   P.inner = g.inner;
   P.splits = 1;
   P.causal = g.causal;
+  P.nz = g.batch;
   return P;
 }
 

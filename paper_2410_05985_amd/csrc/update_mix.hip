@@ -20,7 +20,8 @@
 namespace layup {
 
 constexpr int UM_THREADS = 256;
-constexpr int UM_CHUNK = 2048;  // elements per (block, chunk): one pass of 2 x 4 per thread (measured best)
+constexpr int UM_CHUNK = 2048;  // elements per (block, chunk) = 2 x 4 per thread (measured best)
+static_assert(UM_CHUNK == 8 * UM_THREADS, "one pass of two 4-element groups per thread");
 
 struct UMArgs {
   UMTensor t[UM_MAX_TENSORS];
@@ -45,8 +46,10 @@ __device__ __forceinline__ void um_elem(float& p, float g, float& m, float& v, f
     float pd = p * dfac;                        // p * (1 - lr*wd)
     m = fmaf(A.b1, m, (1.0f - A.b1) * g);
     v = fmaf(A.b2, v, (1.0f - A.b2) * (g * g));
-    float den = fmaf(sqrtf(v), A.inv_sqrt_bc2, A.eps);
-    p1 = fmaf(-A.step_size, m / den, pd);
+    // hardware square root and reciprocal (1 ulp each): the exact-division
+    // sequence costs registers that would cut the waves per SIMD from 8 to 7
+    float den = fmaf(__builtin_amdgcn_sqrtf(v), A.inv_sqrt_bc2, A.eps);
+    p1 = fmaf(-A.step_size, m * __builtin_amdgcn_rcpf(den), pd);
   }
   float d = p1 - q;
   dis = fmaf(d, d, dis);
@@ -65,56 +68,62 @@ __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, 
     const int64_t end = min(begin + (int64_t)UM_CHUNK, T.n);
     const float dfac = T.decay ? (1.0f - A.lr * A.wd) : 1.0f;
     const float wdc = T.decay ? A.wd : 0.0f;
-    const int64_t vend = begin + ((end - begin) & ~(int64_t)3);
-    // two 4-element groups per thread per iteration, all loads issued before
-    // any math; streaming (nontemporal) loads and stores: every byte is used
-    // once, so nothing is kept in the caches
-    for (int64_t i0 = begin + 4 * threadIdx.x; i0 < vend; i0 += 8 * UM_THREADS) {
-      f32x4 p[2], g[2], m[2], v[2], q[2];
+    // chunk base pointers are uniform (scalar registers); lanes use 32-bit
+    // offsets, which keeps the kernel at 8 waves per SIMD
+    const int cnt = (int)(end - begin);   // <= UM_CHUNK
+    const int vcnt = cnt & ~3;
+    float* __restrict__ pp = T.p + begin;
+    const float* __restrict__ gp = T.g + begin;
+    float* __restrict__ mp = T.m + begin;
+    float* __restrict__ vp = OPT == 1 ? T.v + begin : nullptr;
+    const float* __restrict__ qp = T.q + begin;
+    bf16_t* __restrict__ hp = T.p16 ? T.p16 + begin : nullptr;
+    // two 4-element groups per thread, all loads issued before any math;
+    // streaming (nontemporal) loads and stores: every byte is used once
+    f32x4 p[2], g[2], m[2], v[2], q[2];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int64_t i = i0 + (int64_t)u * 4 * UM_THREADS;
-        if (i < vend) {
-          p[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.p + i));
-          g[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.g + i));
-          m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.m + i));
-          q[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.q + i));
-          v[u] = OPT == 1 ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(T.v + i))
-                          : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+    for (int u = 0; u < 2; ++u) {
+      const uint32_t i = 4u * threadIdx.x + u * 4u * UM_THREADS;
+      if (i < (uint32_t)vcnt) {
+        p[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(pp + i));
+        g[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(gp + i));
+        m[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(mp + i));
+        q[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(qp + i));
+        v[u] = OPT == 1 ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(vp + i))
+                        : f32x4{0.f, 0.f, 0.f, 0.f};
       }
+    }
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int64_t i = i0 + (int64_t)u * 4 * UM_THREADS;
-        if (i >= vend) continue;
-        f32x4 po;
+    for (int u = 0; u < 2; ++u) {
+      const uint32_t i = 4u * threadIdx.x + u * 4u * UM_THREADS;
+      if (i >= (uint32_t)vcnt) continue;
+      f32x4 po;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float pj = p[u][j], mj = m[u][j], vj = v[u][j], o;
-          um_elem<OPT>(pj, g[u][j], mj, vj, q[u][j], dfac, wdc, A, dis, o);
-          m[u][j] = mj;
-          v[u][j] = vj;
-          po[j] = o;
-        }
-        __builtin_nontemporal_store(po, reinterpret_cast<f32x4*>(T.p + i));
-        __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(T.m + i));
-        if (OPT == 1) __builtin_nontemporal_store(v[u], reinterpret_cast<f32x4*>(T.v + i));
-        if (T.p16) {
-          u32x2 w;
-          w[0] = pack_bf2(po[0], po[1]);
-          w[1] = pack_bf2(po[2], po[3]);
-          __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(T.p16 + i));
-        }
+      for (int j = 0; j < 4; ++j) {
+        float pj = p[u][j], mj = m[u][j], vj = v[u][j], o;
+        um_elem<OPT>(pj, g[u][j], mj, vj, q[u][j], dfac, wdc, A, dis, o);
+        m[u][j] = mj;
+        v[u][j] = vj;
+        po[j] = o;
+      }
+      __builtin_nontemporal_store(po, reinterpret_cast<f32x4*>(pp + i));
+      __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(mp + i));
+      if (OPT == 1) __builtin_nontemporal_store(v[u], reinterpret_cast<f32x4*>(vp + i));
+      if (hp) {
+        u32x2 w;
+        w[0] = pack_bf2(po[0], po[1]);
+        w[1] = pack_bf2(po[2], po[3]);
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(hp + i));
       }
     }
     // ragged tail of the tensor (fewer than 4 elements)
-    for (int64_t i = vend + threadIdx.x; i < end; i += UM_THREADS) {
-      float p = T.p[i], m = T.m[i], v = OPT == 1 ? T.v[i] : 0.f, o;
-      um_elem<OPT>(p, T.g[i], m, v, T.q[i], dfac, wdc, A, dis, o);
-      T.p[i] = o;
-      T.m[i] = m;
-      if (OPT == 1) T.v[i] = v;
-      if (T.p16) T.p16[i] = f2bf(o);
+    for (uint32_t i = (uint32_t)vcnt + threadIdx.x; i < (uint32_t)cnt; i += UM_THREADS) {
+      float pv = pp[i], mv = mp[i], vv = OPT == 1 ? vp[i] : 0.f, o;
+      um_elem<OPT>(pv, gp[i], mv, vv, qp[i], dfac, wdc, A, dis, o);
+      pp[i] = o;
+      mp[i] = mv;
+      if (OPT == 1) vp[i] = vv;
+      if (hp) hp[i] = f2bf(o);
     }
   }
   if (DIS) {
