@@ -113,18 +113,17 @@ def time_gemms(torch, LU, shapes, reps, stream):
 
 
 def time_update_mix(torch, LU, m, units, hp, alpha, reps, stream):
-    """Average duration of one unit's update+mix launch (AdamW + bf16 copy)
-    with HIP events on the update stream.  The units are launched back to
-    back, one launch per unit, as in the step; the round over all block units
-    (12 x 241 MB for GPT-2-small) is far larger than the 256 MB MALL, so no
+    """Update+mix launches (AdamW + bf16 copy) of the given units, back to
+    back, one launch per unit as in the step, timed with HIP events on the
+    update stream.  Returns the time of one round over the units and, for
+    units of equal size, of one launch.  A round over the 12 GPT-2-small
+    block units moves 12 x 241 MB, far more than the 256 MB MALL, so no
     launch finds its operands in the cache."""
     descs = []
-    numel = None
+    numels = []
     for unit in units:
         t = [x for x in m.infos if x["unit"] == unit]
-        n = sum(x["numel"] for x in t)
-        assert numel is None or n == numel, "units of equal size"
-        numel = n
+        numels.append(sum(x["numel"] for x in t))
         d = []
         for x in t:
             o = x["offset"]
@@ -145,9 +144,19 @@ def time_update_mix(torch, LU, m, units, hp, alpha, reps, stream):
                 LU.layup_layer_update_mix(None, d, hp, alpha, stream=stream)
         e1.record(stream)
     e1.synchronize()
-    ms = e0.elapsed_time(e1) / (reps * len(descs))
-    nbytes = 34 * numel   # AdamW 32 B/param + 2 B bf16 copy
-    return dict(units=len(descs), numel=numel, ms=ms, bytes=nbytes, gbs=nbytes / (ms * 1e-3) / 1e9)
+    round_ms = e0.elapsed_time(e1) / reps
+    nbytes = 34 * sum(numels)   # AdamW 32 B/param + 2 B bf16 copy
+    out = dict(units=len(descs), round_ms=round_ms, round_bytes=nbytes,
+               gbs=nbytes / (round_ms * 1e-3) / 1e9)
+    if len(set(numels)) == 1:
+        out.update(numel=numels[0], ms=round_ms / len(descs), bytes=34 * numels[0])
+    return out
+
+
+def percentiles(xs):
+    xs = sorted(xs)
+    pick = lambda q: xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]
+    return dict(p10=round(pick(0.1), 4), median=round(pick(0.5), 4), p90=round(pick(0.9), 4))
 
 
 def cpu_baseline(cfg_full):
@@ -436,16 +445,48 @@ def main():
         LU.layup_step(model.ctx, td, None, hp, cfg.alpha, 0, loss)
     model.synchronize()
     torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    ev[0].record(model.compute_stream)
+    for i in range(args.steps):
         step += 1
         hp.step = step
         LU.layup_step(model.ctx, td, None, hp, cfg.alpha, 0, loss)
+        ev[i + 1].record(model.compute_stream)   # after the step's join
     model.synchronize()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     loss_v = float(loss.item())
+
+    # forward pass alone (saved activations + loss gradient), compute stream
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    LU.layup_forward(model.ctx, td, None, loss)
+    f0.record(model.compute_stream)
+    for _ in range(args.steps):
+        LU.layup_forward(model.ctx, td, None, loss)
+    f1.record(model.compute_stream)
+    f1.synchronize()
+    fwd_ms = f0.elapsed_time(f1) / args.steps
+
+    # the same step with the update on the compute stream (no overlap)
+    ser = LU.Model(lc, "adamw", two_streams=False)
+    for a, b in ((ser.params, model.params), (ser.m, model.m), (ser.v, model.v), (ser.peers, model.peers)):
+        a.copy_(b)
+    torch.cuda.synchronize()
+    LU.layup_refresh_shadow(ser.ctx)
+    for _ in range(2):
+        LU.layup_step(ser.ctx, td, None, hp, cfg.alpha, 0, loss)
+    s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s0.record(ser.compute_stream)
+    for _ in range(args.steps):
+        LU.layup_step(ser.ctx, td, None, hp, cfg.alpha, 0, loss)
+    s1.record(ser.compute_stream)
+    s1.synchronize()
+    serial_ms = s0.elapsed_time(s1) / args.steps
+    ser.close()
+    del ser
     print(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, loss {loss_v:.4f}", file=sys.stderr,
           flush=True)
 
@@ -457,6 +498,11 @@ def main():
     blk_flops = sum(2.0 * x["M"] * x["N"] * x["K"] for x in g[:len(blk)])
     gemm_tflops = blk_flops / (blk_ms * 1e-3) / 1e12
     um = time_update_mix(torch, LU, model, range(1, cfg.n_layer + 1), hp, cfg.alpha, args.kernel_reps, ks)
+    um_all = time_update_mix(torch, LU, model, range(model.n_units), hp, cfg.alpha, args.kernel_reps, ks)
+    overlap = (serial_ms - ms_step) / um_all["round_ms"]
+    print(f"[bench] step events p10/median/p90 {percentiles(step_ms)}; forward {fwd_ms:.3f} ms; "
+          f"serialized {serial_ms:.3f} ms; update+mix of all {model.n_units} units {um_all['round_ms']:.3f} ms; "
+          f"overlap {overlap:.2f}", file=sys.stderr, flush=True)
     for x in g:
         print(f"[bench] gemm {x['name']:9s} {x['M']}x{x['N']}x{x['K']}: {x['ms']*1e3:8.1f} us "
               f"{x['tflops']:7.1f} TFLOP/s", file=sys.stderr, flush=True)
@@ -498,6 +544,11 @@ def main():
         "backward_gemm_TFLOPs": round(gemm_tflops, 2),
         "head_gemm_TFLOPs": [round(x["tflops"], 1) for x in g[len(blk):]],
         "loss": round(loss_v, 5),
+        "step_ms_events": percentiles(step_ms),
+        "forward_ms": round(fwd_ms, 4),
+        "serialized_ms_per_step": round(serial_ms, 4),
+        "update_mix_all_units_ms": round(um_all["round_ms"], 4),
+        "overlap": round(overlap, 3),
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

@@ -70,20 +70,33 @@ typedef struct {
   int64_t step;
 } layup_hparams;
 
+/* How the locally updated layer p1 meets the peer copy q (Algorithm 1 "Peer
+ * Update", weights alpha = w_sender / (w_sender + w_receiver) of section 3.1):
+ *   LAYUP_MIX_PULL: p <- (1 - alpha) p1 + alpha q; q is read only.  The worker
+ *                   plays the receiver for the peer's copy q after its own
+ *                   local update (one worker with a resident peer buffer).
+ *   LAYUP_MIX_PUSH: p <- p1 and q <- (1 - alpha) q + alpha p1, as Algorithm 1
+ *                   writes it: the sender keeps its update and overwrites the
+ *                   receiving replica's layer (replicas resident on one GPU). */
+typedef enum { LAYUP_MIX_PULL = 0, LAYUP_MIX_PUSH = 1 } layup_mix_mode;
+
 /* One tensor of a layer for the fused update+mix.  All pointers are device
- * pointers, 16-byte aligned.  param/state0/state1/param_bf16 are updated in
- * place; grad and peer are read only; param must alias neither.  state0 is
- * the momentum (SGD) or first moment m (AdamW); state1 the second moment v
- * (AdamW; ignored for SGD).  param_bf16 is an optional bfloat16 copy that is
- * rewritten from the mixed float32 value (may be NULL).  decay selects weight
+ * pointers, 16-byte aligned (bf16 copies 8-byte aligned).
+ * param/state0/state1/param_bf16 are updated in place; grad is read only;
+ * peer is read only in pull mode and mixed in place in push mode; param must
+ * alias neither grad nor peer.  state0 is the momentum (SGD) or first moment m
+ * (AdamW); state1 the second moment v (AdamW; ignored for SGD).  param_bf16 is
+ * an optional bfloat16 copy rewritten from the new float32 param; peer_bf16
+ * (push mode only, nullable) the same for the peer.  decay selects weight
  * decay for this tensor. */
 typedef struct {
   float* param;
   const float* grad;
   float* state0;
   float* state1;
-  const float* peer;
+  float* peer;
   uint16_t* param_bf16;
+  uint16_t* peer_bf16;
   int64_t numel;
   int32_t decay;
   int32_t reserved;
@@ -202,21 +215,92 @@ layup_status layup_unit_update_mix(layup_ctx* ctx, int32_t unit, const layup_hpa
                                    float alpha, int32_t peer_slot, float* disagreement);
 
 /* Fused update+mix of arbitrary tensors (one layer of any model), single pass,
- * HBM bound: reads p, g, m, (v), q once and writes p, m, (v), (p_bf16) once.
+ * HBM bound: reads p, g, m, (v), q once and writes p, m, (v), (p_bf16) once,
+ * and in push mode also q and (q_bf16).  mix_mode is a layup_mix_mode.
  * ctx may be NULL; stream NULL = the context's update stream (or the default
- * stream without a context).  disagreement as above (summed over the
- * tensors).  n_tensors >= 1. */
+ * stream without a context).  disagreement (device float, nullable, needs a
+ * context) receives sum((p_updated - q)^2) summed over the tensors, taken
+ * before the mix (appendix, model disagreement).  n_tensors >= 1. */
 layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
-                                    const layup_hparams* hp, float alpha, float* disagreement,
-                                    void* stream);
+                                    const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                    float* disagreement, void* stream);
 
-/* One whole layer-wise step: forward, then for u = n_units-1 ... 0:
- * layup_layer_backward(u) on the compute stream and
- * layup_unit_update_mix(u) on the update stream, then the compute stream
- * waits for the update stream (join). */
+/* Push-mode update of one unit of the model (Algorithm 1 "Local Update",
+ * "Communication" and "Peer Update" as written): the worker's own layer gets
+ * the local update, then the receiving replica's copy of the layer becomes
+ * (1 - alpha) q + alpha p_updated.  peer_params (device float, flat layout of
+ * this model's configuration) is the receiving replica's parameter buffer,
+ * mixed in place; peer_params_bf16 (nullable) its bfloat16 copy, rewritten
+ * for the mixed elements.  The receiver must not run a step of its own
+ * concurrently.  Otherwise as layup_unit_update_mix. */
+layup_status layup_unit_update_push(layup_ctx* ctx, int32_t unit, const layup_hparams* hp, float alpha,
+                                    float* peer_params, uint16_t* peer_params_bf16,
+                                    float* disagreement);
+
+/* When the unit updates run relative to the backward pass.
+ *   LAYUP_SCHEDULE_LAYERWISE:      update+mix of unit u as soon as its
+ *                                  gradient exists (section 3.2, LayUp),
+ *                                  overlapping the backward of unit u-1.
+ *   LAYUP_SCHEDULE_AFTER_BACKWARD: all units' update+mix after the whole
+ *                                  backward pass (the GoSGD-style schedule
+ *                                  the paper compares against).
+ * On one worker both produce the same numbers (no unit's backward reads a
+ * unit updated before it); they differ in when each update lands. */
+typedef enum { LAYUP_SCHEDULE_LAYERWISE = 0, LAYUP_SCHEDULE_AFTER_BACKWARD = 1 } layup_schedule;
+
+/* Arguments of layup_step_ex. */
+typedef struct {
+  const int32_t* tokens;        /* as layup_forward */
+  const float* x;               /* as layup_forward */
+  const layup_hparams* hp;
+  float alpha;                  /* mixing weight of the peer side */
+  int32_t schedule;             /* layup_schedule */
+  int32_t mix_mode;             /* layup_mix_mode */
+  int32_t peer_slot;            /* pull: resident peer replica */
+  float* push_params;           /* push: receiving replica's params (device) */
+  uint16_t* push_params_bf16;   /* push: its bfloat16 copy (nullable) */
+  float* loss_out;              /* device float scalar, nullable */
+  float* disagreement;          /* device float [n_units], nullable */
+} layup_step_args;
+
+/* One whole step: forward, then for u = n_units-1 ... 0
+ * layup_layer_backward(u) on the compute stream and the unit's update+mix on
+ * the update stream, scheduled as args->schedule says, then the compute
+ * stream waits for the update stream (join).  Records the per-unit timeline
+ * read by layup_unit_timeline. */
+layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* args);
+
+/* layup_step_ex with the layer-wise schedule and pull mode. */
 layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x,
                         const layup_hparams* hp, float alpha, int32_t peer_slot, float* loss_out,
                         float* disagreement /* device [n_units] or NULL */);
+
+/* Timeline of the last completed step of the context (waits for it): for
+ * every unit, the time from the start of the step's forward pass until the
+ * unit's gradient was ready (end of its backward on the compute stream) and
+ * until its update+mix had been applied (end of the launch on the update
+ * stream), in milliseconds, from HIP events.  applied - ready is the delay
+ * with which the unit's update lands, the staleness that the drift model of
+ * section 3.2 counts.  Host arrays of n_units floats.  LAYUP_ERR_STATE if no
+ * whole step has run. */
+layup_status layup_unit_timeline(layup_ctx* ctx, float* ready_ms, float* applied_ms);
+
+/* ------------------------------------------------------------- push-sum */
+
+/* Push-sum weights of the workers (section 3.1): each starts at 1/M; a sender
+ * halves its weight when it sends (Algorithm 1, start of the updater's
+ * round); the receiver mixes the incoming layers with
+ * alpha = w_sender / (w_sender + w_receiver); after the round the receiver's
+ * weight grows by the sender's.  Host arithmetic in double on the caller's
+ * array w[n_workers]; sum(w) is unchanged by a send followed by its receive.
+ *   send:    w[sender] /= 2; *alpha_out = w[sender] / (w[sender] + w[receiver])
+ *   receive: w[receiver] += w[sender]
+ * Errors: null pointers, n_workers < 2, indices out of range, sender ==
+ * receiver, non-positive or non-finite weights (LAYUP_ERR_INVALID_ARG, text
+ * in layup_global_error). */
+layup_status layup_push_sum_send(double* w, int32_t n_workers, int32_t sender, int32_t receiver,
+                                 float* alpha_out);
+layup_status layup_push_sum_receive(double* w, int32_t n_workers, int32_t sender, int32_t receiver);
 
 /* Saved forward activation of the context, for inspection (device pointer
  * into the workspace).  which: 0 = block input x (f32), 1 = LN1 out (bf16),

@@ -216,6 +216,23 @@ def update_mix(p, g, m, v, q, hp: dict, alpha: float, t: int, wd_on=True, store=
     return p2, m1, v1, dis
 
 
+def update_push(p, g, m, v, q, hp: dict, alpha: float, t: int, wd_on=True, store=f32):
+    """Algorithm 1 as written, for one tensor: the sender's "Local Update" of
+    its own copy, then the "Peer Update" of the receiver's copy q with the
+    sent layer, q <- (1 - alpha) q + alpha p1, alpha = w_sender / (w_sender +
+    w_receiver).  Returns float32-rounded (p1, m, v, q_new) and the
+    disagreement between p1 and the receiver's copy before the mix."""
+    if hp["optim"] == "sgd":
+        p1, m1 = sgd_momentum(p, g, m, hp["lr"], hp["momentum"], hp["weight_decay"], wd_on, store)
+        v1 = None
+    else:
+        p1, m1, v1 = adamw(p, g, m, v, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
+                           hp["weight_decay"], t, wd_on, store)
+    dis = disagreement(p1, q)
+    q2 = store(mix(q, p1, alpha))
+    return p1, m1, v1, q2, dis
+
+
 # --------------------------------------------------------- push-sum (host)
 
 
@@ -263,11 +280,20 @@ def gpt_units(n_layer: int) -> List[List[str]]:
     return units
 
 
-def _apply_unit(names, params, grads, m, v, peer, hp, alpha, t, decay_of, store=f32):
+def _apply_unit(names, params, grads, m, v, peer, hp, alpha, t, decay_of, store=f32, push=False):
+    """Update+mix of one unit's tensors.  push=False: the worker's copy
+    absorbs the peer's (``peer`` read only); push=True: the worker keeps its
+    update and the receiver's copy ``peer`` is mixed in place."""
     dis = 0.0
     for n in names:
-        p2, m2, v2, d = update_mix(params[n], grads[n], m[n], None if v is None else v[n],
-                                   peer[n], hp, alpha, t, wd_on=decay_of(n), store=store)
+        vn = None if v is None else v[n]
+        if push:
+            p2, m2, v2, q2, d = update_push(params[n], grads[n], m[n], vn, peer[n], hp, alpha, t,
+                                            wd_on=decay_of(n), store=store)
+            peer[n] = q2
+        else:
+            p2, m2, v2, d = update_mix(params[n], grads[n], m[n], vn, peer[n], hp, alpha, t,
+                                       wd_on=decay_of(n), store=store)
         params[n], m[n] = p2, m2
         if v is not None:
             v[n] = v2
@@ -278,7 +304,7 @@ def _apply_unit(names, params, grads, m, v, peer, hp, alpha, t, decay_of, store=
 # ------------------------------------------------------------ tiny MLP step
 
 
-def mlp_step(params, m, peer, x, y, hp, alpha, t=1, store=f32):
+def mlp_step(params, m, peer, x, y, hp, alpha, t=1, store=f32, push=False):
     """One layer-wise step of the float32 MLP (ReLU between layers, softmax
     cross-entropy, mean over the batch).  Units are the linear layers.
     Returns (loss, grads, trace, disagreements); params and m are updated in
@@ -303,7 +329,7 @@ def mlp_step(params, m, peer, x, y, hp, alpha, t=1, store=f32):
         if u > 0:
             dy = relu_bwd(dx, acts[u])
         dis[u] = _apply_unit(units[u], params, grads, m, None, peer, hp, alpha, t,
-                             lambda n: True, store)
+                             lambda n: True, store, push)
         trace.append(u)
     return loss, grads, trace, dis
 
@@ -406,7 +432,7 @@ def gpt_block_bwd(params, c, dx, l, bsz, t, n_head, rnd: Callable = bf16):
 
 
 def gpt_step(params, m, v, peer, tokens, n_head, hp, alpha, t=1, rnd: Callable = bf16,
-             update: bool = True, store: Callable = f32):
+             update: bool = True, store: Callable = f32, push: bool = False):
     """One layer-wise LayUp step of a GPT stack.  ``params``, ``m``, ``v`` are
     dicts of arrays updated in place (float32 values).  Returns (loss, grads,
     trace, disagreements).  With ``update=False`` only the gradients are
@@ -425,7 +451,7 @@ def gpt_step(params, m, v, peer, tokens, n_head, hp, alpha, t=1, rnd: Callable =
         trace.append(u)
         if update:
             dis[u] = _apply_unit(units[u], params, grads, m, v, peer, hp, alpha, t,
-                                 lambda n: n in decay, store)
+                                 lambda n: n in decay, store, push)
 
     # unit L+1: output head (tied wte) and final LayerNorm
     wte16 = rnd(params_f["wte"])
@@ -447,3 +473,19 @@ def gpt_step(params, m, v, peer, tokens, n_head, hp, alpha, t=1, rnd: Callable =
     grads["wpe"] = store(dx.reshape(bsz, t_len, -1).sum(axis=0))
     apply(0)
     return loss, grads, trace, dis
+
+
+def gpt_update_units(params, grads, m, v, peer, n_layer, hp, alpha, t=1, store: Callable = f32,
+                     push: bool = False):
+    """The update+mix part of a GPT step on given gradients, unit by unit in
+    backward order (Algorithm 1's updater loop over the layers).  With the
+    gradients of a run under test this checks that run's updates on their own
+    inputs.  Returns the trace and the per-unit disagreements."""
+    units = gpt_units(n_layer)
+    decay = {n for n in params if np.ndim(params[n]) >= 2}
+    trace, dis = [], {}
+    for u in reverse_unit_order(len(units)):
+        trace.append(u)
+        dis[u] = _apply_unit(units[u], params, grads, m, v, peer, hp, alpha, t,
+                             lambda n: n in decay, store, push)
+    return trace, dis

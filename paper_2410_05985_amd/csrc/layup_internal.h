@@ -20,8 +20,9 @@ struct UMTensor {
   const float* g;
   float* m;
   float* v;
-  const float* q;
-  bf16_t* p16;
+  float* q;      // peer copy: read (pull) or mixed in place (push)
+  bf16_t* p16;   // bfloat16 copy of p (nullable)
+  bf16_t* q16;   // push: bfloat16 copy of the peer (nullable)
   int64_t n;
   int32_t decay;
   int32_t pad;
@@ -35,9 +36,12 @@ struct TraceInfo {
   int32_t unit = 0;
 };
 
+// push = false: p <- (1-alpha) p1 + alpha q (the worker absorbs the peer);
+// push = true:  p <- p1 and q <- (1-alpha) q + alpha p1 (the worker writes its
+// update into the receiving replica), with p1 the locally updated layer.
 hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp, float alpha,
                              float* dis_out, float* dis_partial, const TraceInfo& tr,
-                             hipStream_t stream);
+                             hipStream_t stream, bool push = false);
 
 // ------------------------------------------------------------------ GEMM
 enum Epilogue : int {

@@ -140,8 +140,11 @@ struct layup_ctx {
   Layout L;
   layup_buffers buf;
   hipStream_t sc = nullptr, su = nullptr;
-  std::vector<hipEvent_t> ev_unit;
+  std::vector<hipEvent_t> ev_unit;     // gradient of unit u ready (compute stream)
+  std::vector<hipEvent_t> ev_applied;  // update+mix of unit u done (update stream)
+  hipEvent_t ev_start = nullptr;       // start of the step's forward pass
   hipEvent_t ev_join = nullptr;
+  bool timeline_valid = false;
   bool have_join = false;
   std::string err;
   int device = 0;
@@ -512,9 +515,10 @@ layup_status mlp_backward(layup_ctx* c, int u) {
 }
 
 // ------------------------------------------------------------ update+mix
-void unit_tensors(layup_ctx* c, int u, int slot, std::vector<UMTensor>& out) {
+// peer: flat buffer of the peer copy (a resident slot or a receiving
+// replica); peer16: its bfloat16 copy (push mode, nullable).
+void unit_tensors(layup_ctx* c, int u, float* peer, bf16_t* peer16, std::vector<UMTensor>& out) {
   out.clear();
-  const float* peer = c->buf.peers + (int64_t)slot * c->L.total;
   for (int ti : c->L.unit_tensors[u]) {
     const TensorInfo& t = c->L.t[ti];
     if (!out.empty()) {
@@ -531,6 +535,7 @@ void unit_tensors(layup_ctx* c, int u, int slot, std::vector<UMTensor>& out) {
     m.v = c->buf.v ? c->buf.v + t.off : nullptr;
     m.q = peer + t.off;
     m.p16 = c->buf.params_bf16 ? c->buf.params_bf16 + t.off : nullptr;
+    m.q16 = peer16 ? peer16 + t.off : nullptr;
     m.n = t.numel;
     m.decay = t.decay;
     m.pad = 0;
@@ -546,16 +551,17 @@ std::string check_hp(const layup_hparams* hp) {
   return "";
 }
 
-layup_status unit_update(layup_ctx* c, int u, const layup_hparams* hp, float alpha, int slot,
-                         float* dis) {
+// Update+mix of unit u against the peer copy `peer` (pull) or into the
+// receiving replica `peer` (push).
+layup_status unit_update(layup_ctx* c, int u, const layup_hparams* hp, float alpha, float* peer,
+                         bf16_t* peer16, bool push, float* dis) {
   std::string m = check_hp(hp);
   if (!m.empty()) return fail(c, LAYUP_ERR_INVALID_ARG, m);
   if (u < 0 || u >= c->L.n_units) return fail(c, LAYUP_ERR_INVALID_ARG, "unit index out of range");
-  if (slot < 0 || slot >= c->cfg.n_peers) return fail(c, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
   if (hp->kind == LAYUP_ADAMW && !c->buf.v) return fail(c, LAYUP_ERR_INVALID_ARG, "AdamW needs the v buffer");
   if (!c->backward_done[u]) return fail(c, LAYUP_ERR_STATE, "unit updated before its backward");
   std::vector<UMTensor> ts;
-  unit_tensors(c, u, slot, ts);
+  unit_tensors(c, u, peer, peer16, ts);
   HIPCHK(c, hipStreamWaitEvent(c->su, c->ev_unit[u], 0), "wait for unit gradient");
   TraceInfo tr;
   tr.trace = c->buf.trace;
@@ -567,16 +573,35 @@ layup_status unit_update(layup_ctx* c, int u, const layup_hparams* hp, float alp
     int n = (int)std::min<size_t>(UM_MAX_TENSORS, ts.size() - i);
     TraceInfo t2 = tr;
     if (i > 0) t2.trace = nullptr;  // one trace entry per unit
-    HIPCHK(c, launch_update_mix(&ts[i], n, *hp, alpha, (i == 0) ? dis : nullptr, c->dis_partial, t2, c->su),
+    HIPCHK(c, launch_update_mix(&ts[i], n, *hp, alpha, (i == 0) ? dis : nullptr, c->dis_partial, t2, c->su,
+                                push),
            "update+mix");
   }
+  HIPCHK(c, hipEventRecord(c->ev_applied[u], c->su), "record unit applied");
   c->backward_done[u] = 0;
   if (u == 0) {
     HIPCHK(c, hipEventRecord(c->ev_join, c->su), "record join");
     c->have_join = true;
+    c->timeline_valid = true;
     c->step_index++;
   }
   return LAYUP_OK;
+}
+
+float* slot_ptr(layup_ctx* c, int slot) {
+  return const_cast<float*>(c->buf.peers) + (int64_t)slot * c->L.total;
+}
+
+// push target checks: a whole flat buffer of this configuration that is not
+// one of the context's own
+std::string check_push_target(layup_ctx* c, const float* peer, const uint16_t* peer16) {
+  if (!peer) return "push mode needs the receiving replica's parameters";
+  if ((uintptr_t)peer & 15) return "receiving replica must be 16-byte aligned";
+  if ((uintptr_t)peer16 & 7) return "receiving replica's bf16 copy must be 8-byte aligned";
+  const float* own = c->buf.params;
+  if (peer < own + c->L.total && own < peer + c->L.total)
+    return "receiving replica overlaps the worker's own parameters";
+  return "";
 }
 
 }  // namespace
@@ -660,14 +685,17 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
   c->su = update_stream ? (hipStream_t)update_stream : c->sc;
   hipGetDevice(&c->device);
   c->ev_unit.assign(c->L.n_units, nullptr);
+  c->ev_applied.assign(c->L.n_units, nullptr);
   c->backward_done.assign(c->L.n_units, 0);
-  for (auto& e : c->ev_unit) {
-    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+  // unit events carry timestamps (the per-unit timeline); the join does not
+  for (int u = 0; u < c->L.n_units; ++u) {
+    if (hipEventCreate(&c->ev_unit[u]) != hipSuccess || hipEventCreate(&c->ev_applied[u]) != hipSuccess) {
       layup_destroy(c);
       return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
     }
   }
-  if (hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
+  if (hipEventCreate(&c->ev_start) != hipSuccess ||
+      hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
     layup_destroy(c);
     return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
   }
@@ -679,6 +707,9 @@ void layup_destroy(layup_ctx* ctx) {
   if (!ctx) return;
   for (auto e : ctx->ev_unit)
     if (e) hipEventDestroy(e);
+  for (auto e : ctx->ev_applied)
+    if (e) hipEventDestroy(e);
+  if (ctx->ev_start) hipEventDestroy(ctx->ev_start);
   if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
   delete ctx;
 }
@@ -707,6 +738,8 @@ layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x
     if (b) return fail(ctx, LAYUP_ERR_STATE, "forward called while a unit awaits its update");
   // the forward reads every unit's weights: wait for the previous step's updates
   if (ctx->have_join) HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "wait join");
+  HIPCHK(ctx, hipEventRecord(ctx->ev_start, ctx->sc), "record step start");
+  ctx->timeline_valid = false;
   ctx->tokens = tokens;
   layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_forward(ctx, tokens, loss_out)
                                                             : mlp_forward(ctx, tokens, x, loss_out);
@@ -734,13 +767,26 @@ layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit) {
 layup_status layup_unit_update_mix(layup_ctx* ctx, int32_t unit, const layup_hparams* hp, float alpha,
                                    int32_t peer_slot, float* disagreement) {
   if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
-  return unit_update(ctx, unit, hp, alpha, peer_slot, disagreement);
+  if (peer_slot < 0 || peer_slot >= ctx->cfg.n_peers)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
+  return unit_update(ctx, unit, hp, alpha, slot_ptr(ctx, peer_slot), nullptr, false, disagreement);
+}
+
+layup_status layup_unit_update_push(layup_ctx* ctx, int32_t unit, const layup_hparams* hp, float alpha,
+                                    float* peer_params, uint16_t* peer_params_bf16, float* disagreement) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  std::string m = check_push_target(ctx, peer_params, peer_params_bf16);
+  if (!m.empty()) return fail(ctx, m.find("aligned") != std::string::npos ? LAYUP_ERR_ALIGN : LAYUP_ERR_INVALID_ARG, m);
+  return unit_update(ctx, unit, hp, alpha, peer_params, peer_params_bf16, true, disagreement);
 }
 
 layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
-                                    const layup_hparams* hp, float alpha, float* disagreement,
-                                    void* stream) {
+                                    const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                    float* disagreement, void* stream) {
   if (!tensors || n_tensors < 1) return fail(ctx, LAYUP_ERR_INVALID_ARG, "no tensors");
+  if (mix_mode != LAYUP_MIX_PULL && mix_mode != LAYUP_MIX_PUSH)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown mix mode");
+  const bool push = mix_mode == LAYUP_MIX_PUSH;
   std::string m = check_hp(hp);
   if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
   if (disagreement && !ctx)
@@ -755,7 +801,8 @@ layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors,
     uintptr_t al = (uintptr_t)t.param | (uintptr_t)t.grad | (uintptr_t)t.state0 | (uintptr_t)t.peer |
                    (uintptr_t)(hp->kind == LAYUP_ADAMW ? t.state1 : nullptr);
     if (al & 15) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": pointers must be 16-byte aligned");
-    if ((uintptr_t)t.param_bf16 & 7) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": bf16 copy must be 8-byte aligned");
+    if (((uintptr_t)t.param_bf16 | (uintptr_t)(push ? t.peer_bf16 : nullptr)) & 7)
+      return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": bf16 copies must be 8-byte aligned");
     if ((const void*)t.param == (const void*)t.peer || (const void*)t.param == (const void*)t.grad)
       return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": param aliases grad or peer");
     UMTensor& u = ts[i];
@@ -765,6 +812,7 @@ layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors,
     u.v = hp->kind == LAYUP_ADAMW ? t.state1 : nullptr;
     u.q = t.peer;
     u.p16 = t.param_bf16;
+    u.q16 = push ? t.peer_bf16 : nullptr;
     u.n = t.numel;
     u.decay = t.decay ? 1 : 0;
     u.pad = 0;
@@ -776,25 +824,102 @@ layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors,
     return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
   for (int i = 0; i < n_tensors; i += UM_MAX_TENSORS) {
     int n = std::min(UM_MAX_TENSORS, n_tensors - i);
-    hipError_t e = launch_update_mix(&ts[i], n, *hp, alpha, disagreement, part, tr, s);
+    hipError_t e = launch_update_mix(&ts[i], n, *hp, alpha, disagreement, part, tr, s, push);
     if (e != hipSuccess) return hip_fail(ctx, e, "update+mix");
   }
   return LAYUP_OK;
 }
 
-layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x, const layup_hparams* hp,
-                        float alpha, int32_t peer_slot, float* loss_out, float* disagreement) {
+layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* a) {
   if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
-  std::string m = check_hp(hp);
+  if (!a) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null step arguments");
+  std::string m = check_hp(a->hp);
   if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
-  if (peer_slot < 0 || peer_slot >= ctx->cfg.n_peers) return fail(ctx, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
-  TRY(layup_forward(ctx, tokens, x, loss_out));
-  for (int u = ctx->L.n_units - 1; u >= 0; --u) {
-    TRY(layup_layer_backward(ctx, u));
-    TRY(unit_update(ctx, u, hp, alpha, peer_slot, disagreement ? disagreement + u : nullptr));
+  if (a->schedule != LAYUP_SCHEDULE_LAYERWISE && a->schedule != LAYUP_SCHEDULE_AFTER_BACKWARD)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown schedule");
+  float* peer = nullptr;
+  bf16_t* peer16 = nullptr;
+  const bool push = a->mix_mode == LAYUP_MIX_PUSH;
+  if (a->mix_mode == LAYUP_MIX_PULL) {
+    if (a->peer_slot < 0 || a->peer_slot >= ctx->cfg.n_peers)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "peer slot out of range");
+    peer = slot_ptr(ctx, a->peer_slot);
+  } else if (push) {
+    m = check_push_target(ctx, a->push_params, a->push_params_bf16);
+    if (!m.empty()) return fail(ctx, m.find("aligned") != std::string::npos ? LAYUP_ERR_ALIGN : LAYUP_ERR_INVALID_ARG, m);
+    peer = a->push_params;
+    peer16 = a->push_params_bf16;
+  } else {
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown mix mode");
+  }
+  TRY(layup_forward(ctx, a->tokens, a->x, a->loss_out));
+  const int U = ctx->L.n_units;
+  auto dis = [&](int u) { return a->disagreement ? a->disagreement + u : nullptr; };
+  if (a->schedule == LAYUP_SCHEDULE_LAYERWISE) {
+    for (int u = U - 1; u >= 0; --u) {
+      TRY(layup_layer_backward(ctx, u));
+      TRY(unit_update(ctx, u, a->hp, a->alpha, peer, peer16, push, dis(u)));
+    }
+  } else {
+    for (int u = U - 1; u >= 0; --u) TRY(layup_layer_backward(ctx, u));
+    // every update waits for the end of the whole backward pass (unit 0's
+    // gradient is the last one produced)
+    HIPCHK(ctx, hipStreamWaitEvent(ctx->su, ctx->ev_unit[0], 0), "wait for the end of the backward pass");
+    for (int u = U - 1; u >= 0; --u) TRY(unit_update(ctx, u, a->hp, a->alpha, peer, peer16, push, dis(u)));
   }
   // join: the compute stream continues only after the last update
   HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "join");
+  return LAYUP_OK;
+}
+
+layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x, const layup_hparams* hp,
+                        float alpha, int32_t peer_slot, float* loss_out, float* disagreement) {
+  layup_step_args a;
+  memset(&a, 0, sizeof(a));
+  a.tokens = tokens;
+  a.x = x;
+  a.hp = hp;
+  a.alpha = alpha;
+  a.schedule = LAYUP_SCHEDULE_LAYERWISE;
+  a.mix_mode = LAYUP_MIX_PULL;
+  a.peer_slot = peer_slot;
+  a.loss_out = loss_out;
+  a.disagreement = disagreement;
+  return layup_step_ex(ctx, &a);
+}
+
+layup_status layup_unit_timeline(layup_ctx* ctx, float* ready_ms, float* applied_ms) {
+  if (!ctx || !ready_ms || !applied_ms) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null argument");
+  if (!ctx->timeline_valid) return fail(ctx, LAYUP_ERR_STATE, "no whole step has run since the last forward");
+  TRY(layup_synchronize(ctx));
+  for (int u = 0; u < ctx->L.n_units; ++u) {
+    HIPCHK(ctx, hipEventElapsedTime(&ready_ms[u], ctx->ev_start, ctx->ev_unit[u]), "unit ready time");
+    HIPCHK(ctx, hipEventElapsedTime(&applied_ms[u], ctx->ev_start, ctx->ev_applied[u]), "unit applied time");
+  }
+  return LAYUP_OK;
+}
+
+layup_status layup_push_sum_send(double* w, int32_t n_workers, int32_t sender, int32_t receiver,
+                                 float* alpha_out) {
+  if (!w || !alpha_out) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null argument");
+  if (n_workers < 2) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "push-sum needs at least two workers");
+  if (sender < 0 || sender >= n_workers || receiver < 0 || receiver >= n_workers)
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "worker index out of range");
+  if (sender == receiver) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "a worker does not send to itself");
+  if (!(w[sender] > 0.0) || !(w[receiver] > 0.0) || !std::isfinite(w[sender]) || !std::isfinite(w[receiver]))
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "push-sum weights must be positive and finite");
+  w[sender] *= 0.5;
+  *alpha_out = (float)(w[sender] / (w[sender] + w[receiver]));
+  return LAYUP_OK;
+}
+
+layup_status layup_push_sum_receive(double* w, int32_t n_workers, int32_t sender, int32_t receiver) {
+  if (!w) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null argument");
+  if (n_workers < 2) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "push-sum needs at least two workers");
+  if (sender < 0 || sender >= n_workers || receiver < 0 || receiver >= n_workers)
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "worker index out of range");
+  if (sender == receiver) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "a worker does not send to itself");
+  w[receiver] += w[sender];
   return LAYUP_OK;
 }
 

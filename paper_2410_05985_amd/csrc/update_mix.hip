@@ -6,15 +6,19 @@
 // or AdamW (decoupled decay, bias-corrected):
 //   p' = p*(1 - lr*wd);  m = b1*m + (1-b1)*g;  v = b2*v + (1-b2)*g*g;
 //   p1 = p' - (lr/bc1) * m / (sqrt(v)/sqrt(bc2) + eps)
-// then the peer average  p2 = a*p1 + b*q  with a = 1-alpha, b = alpha, and
-// optionally the bfloat16 copy of p2 and the disagreement sum((p1-q)^2).
+// then the peer average with a = 1-alpha, b = alpha, in one of two forms:
+//   pull:  p2 = a*p1 + b*q          (the worker's copy absorbs the peer's)
+//   push:  p2 = p1, q2 = a*q + b*p1 (Algorithm 1 as written: the sender keeps
+//          its update and overwrites the receiving replica's layer)
+// optionally the bfloat16 copies of the written tensors and the disagreement
+// sum((p1-q)^2).
 //
 // Each tensor is read once and written once (streaming loads and stores):
-// 24 B/param for SGD momentum
-// (read p,g,m,q; write p,m), 32 B/param for AdamW (read p,g,m,v,q; write
-// p,m,v), +2 B with the bfloat16 copy.  Loads and stores are 128-bit; the
-// grid walks (tensor, chunk) pairs of a multi-tensor table so a layer of many
-// small tensors is one launch.
+// pull 24 B/param for SGD momentum (read p,g,m,q; write p,m), 32 B/param for
+// AdamW (read p,g,m,v,q; write p,m,v), +2 B with the bfloat16 copy; push adds
+// the write of q (+4 B) and its bfloat16 copy (+2 B).  Loads and stores are
+// 128-bit; the grid walks (tensor, chunk) pairs of a multi-tensor table so a
+// layer of many small tensors is one launch.
 #include "layup_internal.h"
 
 namespace layup {
@@ -34,9 +38,10 @@ struct UMArgs {
   int32_t* trace_counter;
 };
 
-template <int OPT>
+template <int OPT, bool PUSH>
 __device__ __forceinline__ void um_elem(float& p, float g, float& m, float& v, float q, float dfac,
-                                        float wdc, const UMArgs& A, float& dis, float& p_out) {
+                                        float wdc, const UMArgs& A, float& dis, float& p_out,
+                                        float& q_out) {
   float p1;
   if (OPT == 0) {
     float gg = fmaf(wdc, p, g);                 // g + wd*p (wdc = 0 without decay)
@@ -53,10 +58,16 @@ __device__ __forceinline__ void um_elem(float& p, float g, float& m, float& v, f
   }
   float d = p1 - q;
   dis = fmaf(d, d, dis);
-  p_out = fmaf(A.a, p1, A.b * q);
+  if (PUSH) {
+    p_out = p1;
+    q_out = fmaf(A.a, q, A.b * p1);
+  } else {
+    p_out = fmaf(A.a, p1, A.b * q);
+    q_out = q;
+  }
 }
 
-template <int OPT, bool DIS>
+template <int OPT, bool DIS, bool PUSH>
 __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, int64_t total_chunks) {
   __shared__ float red[16];
   float dis = 0.f;
@@ -76,8 +87,9 @@ __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, 
     const float* __restrict__ gp = T.g + begin;
     float* __restrict__ mp = T.m + begin;
     float* __restrict__ vp = OPT == 1 ? T.v + begin : nullptr;
-    const float* __restrict__ qp = T.q + begin;
+    float* __restrict__ qp = T.q + begin;
     bf16_t* __restrict__ hp = T.p16 ? T.p16 + begin : nullptr;
+    bf16_t* __restrict__ hq = PUSH && T.q16 ? T.q16 + begin : nullptr;
     // two 4-element groups per thread, all loads issued before any math;
     // streaming (nontemporal) loads and stores: every byte is used once
     f32x4 p[2], g[2], m[2], v[2], q[2];
@@ -97,16 +109,26 @@ __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, 
     for (int u = 0; u < 2; ++u) {
       const uint32_t i = 4u * threadIdx.x + u * 4u * UM_THREADS;
       if (i >= (uint32_t)vcnt) continue;
-      f32x4 po;
+      f32x4 po, qo;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        float pj = p[u][j], mj = m[u][j], vj = v[u][j], o;
-        um_elem<OPT>(pj, g[u][j], mj, vj, q[u][j], dfac, wdc, A, dis, o);
+        float pj = p[u][j], mj = m[u][j], vj = v[u][j], o, oq;
+        um_elem<OPT, PUSH>(pj, g[u][j], mj, vj, q[u][j], dfac, wdc, A, dis, o, oq);
         m[u][j] = mj;
         v[u][j] = vj;
         po[j] = o;
+        qo[j] = oq;
       }
       __builtin_nontemporal_store(po, reinterpret_cast<f32x4*>(pp + i));
+      if (PUSH) {
+        __builtin_nontemporal_store(qo, reinterpret_cast<f32x4*>(qp + i));
+        if (hq) {
+          u32x2 w;
+          w[0] = pack_bf2(qo[0], qo[1]);
+          w[1] = pack_bf2(qo[2], qo[3]);
+          __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(hq + i));
+        }
+      }
       __builtin_nontemporal_store(m[u], reinterpret_cast<f32x4*>(mp + i));
       if (OPT == 1) __builtin_nontemporal_store(v[u], reinterpret_cast<f32x4*>(vp + i));
       if (hp) {
@@ -118,9 +140,13 @@ __global__ __launch_bounds__(UM_THREADS) void update_mix_kernel(const UMArgs A, 
     }
     // ragged tail of the tensor (fewer than 4 elements)
     for (uint32_t i = (uint32_t)vcnt + threadIdx.x; i < (uint32_t)cnt; i += UM_THREADS) {
-      float pv = pp[i], mv = mp[i], vv = OPT == 1 ? vp[i] : 0.f, o;
-      um_elem<OPT>(pv, gp[i], mv, vv, qp[i], dfac, wdc, A, dis, o);
+      float pv = pp[i], mv = mp[i], vv = OPT == 1 ? vp[i] : 0.f, o, oq;
+      um_elem<OPT, PUSH>(pv, gp[i], mv, vv, qp[i], dfac, wdc, A, dis, o, oq);
       pp[i] = o;
+      if (PUSH) {
+        qp[i] = oq;
+        if (hq) hq[i] = f2bf(oq);
+      }
       mp[i] = mv;
       if (OPT == 1) vp[i] = vv;
       if (hp) hp[i] = f2bf(o);
@@ -151,9 +177,15 @@ __global__ void sum_partials_kernel(const float* part, int n, float* out) {
 
 int64_t update_mix_max_blocks() { return UM_MAX_BLOCKS; }
 
+template <int OPT, bool DIS>
+static void launch_um(bool push, int64_t grid, const UMArgs& A, int64_t chunks, hipStream_t stream) {
+  if (push) update_mix_kernel<OPT, DIS, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+  else update_mix_kernel<OPT, DIS, false><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+}
+
 hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp, float alpha,
                              float* dis_out, float* dis_partial, const TraceInfo& tr,
-                             hipStream_t stream) {
+                             hipStream_t stream, bool push) {
   UMArgs A;
   memset(&A, 0, sizeof(A));
   int64_t chunks = 0;
@@ -189,11 +221,11 @@ hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp,
   int64_t grid = std::min<int64_t>(chunks, UM_MAX_BLOCKS);
   const bool dis = dis_out != nullptr;
   if (hp.kind == LAYUP_ADAMW) {
-    if (dis) update_mix_kernel<1, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
-    else update_mix_kernel<1, false><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+    if (dis) launch_um<1, true>(push, grid, A, chunks, stream);
+    else launch_um<1, false>(push, grid, A, chunks, stream);
   } else {
-    if (dis) update_mix_kernel<0, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
-    else update_mix_kernel<0, false><<<grid, UM_THREADS, 0, stream>>>(A, chunks);
+    if (dis) launch_um<0, true>(push, grid, A, chunks, stream);
+    else launch_um<0, false>(push, grid, A, chunks, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

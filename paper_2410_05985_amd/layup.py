@@ -21,6 +21,8 @@ LAYUP_OK, LAYUP_ERR_INVALID_ARG, LAYUP_ERR_SHAPE, LAYUP_ERR_ALIGN, LAYUP_ERR_DTY
 LAYUP_SGD_MOMENTUM, LAYUP_ADAMW = 0, 1
 LAYUP_MODEL_MLP_F32, LAYUP_MODEL_GPT_BF16 = 0, 1
 LAYUP_MAX_MLP_LAYERS = 8
+LAYUP_MIX_PULL, LAYUP_MIX_PUSH = 0, 1
+LAYUP_SCHEDULE_LAYERWISE, LAYUP_SCHEDULE_AFTER_BACKWARD = 0, 1
 
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "SHAPE", 3: "ALIGN", 4: "DTYPE", 5: "STATE", 6: "HIP"}
 
@@ -34,7 +36,8 @@ class layup_hparams(C.Structure):
 class layup_tensor(C.Structure):
     _fields_ = [("param", C.c_void_p), ("grad", C.c_void_p), ("state0", C.c_void_p),
                 ("state1", C.c_void_p), ("peer", C.c_void_p), ("param_bf16", C.c_void_p),
-                ("numel", C.c_int64), ("decay", C.c_int32), ("reserved", C.c_int32)]
+                ("peer_bf16", C.c_void_p), ("numel", C.c_int64), ("decay", C.c_int32),
+                ("reserved", C.c_int32)]
 
 
 class layup_config(C.Structure):
@@ -58,6 +61,13 @@ class layup_buffers(C.Structure):
                 ("trace_capacity", C.c_int32), ("reserved", C.c_int32)]
 
 
+class layup_step_args(C.Structure):
+    _fields_ = [("tokens", C.c_void_p), ("x", C.c_void_p), ("hp", C.c_void_p), ("alpha", C.c_float),
+                ("schedule", C.c_int32), ("mix_mode", C.c_int32), ("peer_slot", C.c_int32),
+                ("push_params", C.c_void_p), ("push_params_bf16", C.c_void_p),
+                ("loss_out", C.c_void_p), ("disagreement", C.c_void_p)]
+
+
 class layup_gemm_desc(C.Structure):
     _fields_ = [("a_kmajor", C.c_int32), ("b_kmajor", C.c_int32),
                 ("M", C.c_int64), ("N", C.c_int64), ("K", C.c_int64),
@@ -75,8 +85,9 @@ EXPORTS = [
     "layup_param_layout", "layup_tensor_layout", "layup_workspace_size", "layup_init",
     "layup_destroy", "layup_last_error", "layup_global_error", "layup_synchronize",
     "layup_refresh_shadow", "layup_forward", "layup_layer_backward", "layup_unit_update_mix",
-    "layup_layer_update_mix", "layup_step", "layup_activation", "layup_gemm_bf16",
-    "layup_gemm_f32",
+    "layup_layer_update_mix", "layup_unit_update_push", "layup_step_ex", "layup_step",
+    "layup_unit_timeline", "layup_push_sum_send", "layup_push_sum_receive", "layup_activation",
+    "layup_gemm_bf16", "layup_gemm_f32",
 ]
 
 _lib: Optional[C.CDLL] = None
@@ -105,8 +116,13 @@ def lib() -> C.CDLL:
         "layup_forward": ([P, P, P, P], C.c_int),
         "layup_layer_backward": ([P, C.c_int32], C.c_int),
         "layup_unit_update_mix": ([P, C.c_int32, P, C.c_float, C.c_int32, P], C.c_int),
-        "layup_layer_update_mix": ([P, P, C.c_int32, P, C.c_float, P, P], C.c_int),
+        "layup_layer_update_mix": ([P, P, C.c_int32, P, C.c_float, C.c_int32, P, P], C.c_int),
+        "layup_unit_update_push": ([P, C.c_int32, P, C.c_float, P, P, P], C.c_int),
+        "layup_step_ex": ([P, P], C.c_int),
         "layup_step": ([P, P, P, P, C.c_float, C.c_int32, P, P], C.c_int),
+        "layup_unit_timeline": ([P, P, P], C.c_int),
+        "layup_push_sum_send": ([P, C.c_int32, C.c_int32, C.c_int32, P], C.c_int),
+        "layup_push_sum_receive": ([P, C.c_int32, C.c_int32, C.c_int32], C.c_int),
         "layup_activation": ([P, C.c_int32, C.c_int32, P, P, P], C.c_int),
         "layup_gemm_bf16": ([P, P], C.c_int),
         "layup_gemm_f32": ([P, P], C.c_int),
@@ -235,10 +251,48 @@ def layup_unit_update_mix(ctx, unit: int, hp: layup_hparams, alpha: float, peer_
 
 
 def layup_layer_update_mix(ctx, tensors: List[layup_tensor], hp: layup_hparams, alpha: float,
-                           disagreement=None, stream=None):
+                           disagreement=None, stream=None, mix_mode: int = LAYUP_MIX_PULL):
     arr = (layup_tensor * len(tensors))(*tensors)
-    _check(lib().layup_layer_update_mix(ctx, arr, len(tensors), C.byref(hp), alpha,
+    _check(lib().layup_layer_update_mix(ctx, arr, len(tensors), C.byref(hp), alpha, mix_mode,
                                         _ptr(disagreement), _stream(stream)), ctx)
+
+
+def layup_unit_update_push(ctx, unit: int, hp: layup_hparams, alpha: float, peer_params,
+                           peer_params_bf16=None, disagreement=None):
+    _check(lib().layup_unit_update_push(ctx, unit, C.byref(hp), alpha, _ptr(peer_params),
+                                        _ptr(peer_params_bf16), _ptr(disagreement)), ctx)
+
+
+def layup_step_ex(ctx, tokens, x, hp: layup_hparams, alpha: float, schedule: int = LAYUP_SCHEDULE_LAYERWISE,
+                  mix_mode: int = LAYUP_MIX_PULL, peer_slot: int = 0, push_params=None,
+                  push_params_bf16=None, loss_out=None, disagreement=None):
+    a = layup_step_args()
+    a.tokens, a.x = _ptr(tokens), _ptr(x)
+    a.hp = C.addressof(hp)
+    a.alpha, a.schedule, a.mix_mode, a.peer_slot = alpha, schedule, mix_mode, peer_slot
+    a.push_params, a.push_params_bf16 = _ptr(push_params), _ptr(push_params_bf16)
+    a.loss_out, a.disagreement = _ptr(loss_out), _ptr(disagreement)
+    _check(lib().layup_step_ex(ctx, C.byref(a)), ctx)
+
+
+def layup_unit_timeline(ctx, n_units: int):
+    """(ready_ms, applied_ms) lists of the last whole step."""
+    r, a = (C.c_float * n_units)(), (C.c_float * n_units)()
+    _check(lib().layup_unit_timeline(ctx, r, a), ctx)
+    return list(r), list(a)
+
+
+def layup_push_sum_send(w, sender: int, receiver: int) -> float:
+    """w: numpy float64 array of the workers' weights, updated in place."""
+    assert w.dtype == np.float64 and w.flags.c_contiguous
+    alpha = C.c_float()
+    _check(lib().layup_push_sum_send(w.ctypes.data, len(w), sender, receiver, C.byref(alpha)))
+    return alpha.value
+
+
+def layup_push_sum_receive(w, sender: int, receiver: int):
+    assert w.dtype == np.float64 and w.flags.c_contiguous
+    _check(lib().layup_push_sum_receive(w.ctypes.data, len(w), sender, receiver))
 
 
 def layup_step(ctx, tokens, x, hp: layup_hparams, alpha: float, peer_slot: int = 0, loss_out=None,
@@ -286,7 +340,7 @@ class Model:
     the flat buffers and reading tensors back is plain memory plumbing."""
 
     def __init__(self, cfg: layup_config, optim: str, device="cuda", two_streams: bool = True,
-                 trace_capacity: int = 4096):
+                 trace_capacity: int = 4096, workspace=None, streams=None):
         import torch
         self.torch = torch
         self.cfg = cfg
@@ -305,9 +359,15 @@ class Model:
         self.trace = torch.zeros(2 * trace_capacity, dtype=torch.int32, device=device)
         self.trace_counter = torch.zeros(1, dtype=torch.int32, device=device)
         self.ws_bytes = layup_workspace_size(cfg)
-        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
-        self.compute_stream = torch.cuda.Stream(device=device)
-        self.update_stream = torch.cuda.Stream(device=device) if two_streams else self.compute_stream
+        # a workspace may be shared by contexts whose steps never overlap
+        self.workspace = workspace if workspace is not None else \
+            torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        if streams is not None:
+            # contexts on one pair of streams run their steps in call order
+            self.compute_stream, self.update_stream = streams
+        else:
+            self.compute_stream = torch.cuda.Stream(device=device)
+            self.update_stream = torch.cuda.Stream(device=device) if two_streams else self.compute_stream
         b = layup_buffers()
         b.params, b.grads, b.m = _ptr(self.params), _ptr(self.grads), _ptr(self.m)
         b.v = _ptr(self.v)

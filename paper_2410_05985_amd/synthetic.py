@@ -237,6 +237,19 @@ def peer_slots(n_steps: int, n_peers: int, seed: int = 3) -> np.ndarray:
     return rng.integers(0, n_peers, n_steps).astype(np.int32)
 
 
+def gossip_pairs(n_steps: int, n_workers: int, seed: int = 4) -> List[Tuple[int, int]]:
+    """(sender, receiver) per step for replicas that take their steps in turn:
+    step s belongs to worker s mod M, whose receiver is drawn uniformly from
+    the other M-1 workers."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for s in range(n_steps):
+        i = s % n_workers
+        r = int(rng.integers(0, n_workers - 1))
+        out.append((i, r if r < i else r + 1))
+    return out
+
+
 def resnet50_tensors():
     """Returns (params, grads, peer) dicts for the ResNet-50 update+mix sweep."""
     specs = resnet50_param_specs()

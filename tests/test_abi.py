@@ -131,3 +131,56 @@ def test_update_mix_argument_checks_need_no_gpu():
     with pytest.raises(LU.LayupError) as e:      # disagreement without a context
         LU.layup_layer_update_mix(None, [t], hp, 0.5, disagreement=0x6000)
     assert e.value.status == LU.LAYUP_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------- push-sum (host)
+
+def test_push_sum_host_functions_match_oracle(L):
+    """layup_push_sum_send / _receive (host arithmetic in the library) follow
+    the oracle's push-sum exchange exactly over a long random sequence: the
+    same weights bit for bit, alpha equal to the oracle's rounded to float32,
+    total weight 1."""
+    import numpy as np
+    import oracle as O
+    rng = np.random.default_rng(11)
+    M = 5
+    w = np.full(M, 1.0 / M)
+    wo = [1.0 / M] * M
+    for _ in range(500):
+        i = int(rng.integers(M))
+        j = int((i + 1 + rng.integers(M - 1)) % M)
+        alpha = LU.layup_push_sum_send(w, i, j)
+        LU.layup_push_sum_receive(w, i, j)
+        wo, ao = O.push_sum_round(wo, i, j)
+        assert alpha == float(np.float32(ao))
+        assert list(w) == wo
+        assert abs(w.sum() - 1.0) < 1e-12
+
+
+def test_push_sum_golden_exchange(L):
+    """The worked two-worker exchange: weights 1/2 each, the sender halves to
+    1/4, alpha = 1/3, the receiver ends at 3/4."""
+    import json
+    import numpy as np
+    c = json.load(open(os.path.join(ROOT, "tests", "golden", "hand_2x2.json")))["push_sum_exchange"]
+    w = np.array(c["w"], dtype=np.float64)
+    alpha = LU.layup_push_sum_send(w, c["sender"], c["receiver"])
+    assert alpha == float(np.float32(c["alpha"]))
+    LU.layup_push_sum_receive(w, c["sender"], c["receiver"])
+    assert list(w) == c["w_after"]
+
+
+def test_push_sum_rejects_bad_arguments(L):
+    import numpy as np
+    w = np.full(3, 1.0 / 3)
+    for args in ((0, 0), (-1, 1), (0, 3)):
+        with pytest.raises(LU.LayupError):
+            LU.layup_push_sum_send(w, *args)
+        with pytest.raises(LU.LayupError):
+            LU.layup_push_sum_receive(w, *args)
+    with pytest.raises(LU.LayupError):
+        LU.layup_push_sum_send(np.full(1, 1.0), 0, 0)
+    bad = np.array([0.5, 0.0, 0.5])
+    with pytest.raises(LU.LayupError):
+        LU.layup_push_sum_send(bad, 0, 1)
+    assert list(w) == [1.0 / 3] * 3   # nothing changed by the rejected calls
