@@ -20,6 +20,8 @@ Other workloads (one JSON line each, not the default bench line):
   --workload resnet50-update  update+mix sweep over the 161 ResNet-50
                            tensors (54 units in reverse order), SGD momentum
   --workload mlp           tiny float32 MLP, 10 layer-wise steps
+  --workload gossip        4 GPT-2-small replicas resident on the GPU taking
+                           steps in turn, push mode with push-sum weights
   --workload kernels       one launch each of: a 1 GiB copy (counter
                            calibration), one GPT-2-small block's 8 backward
                            GEMMs, one block's update+mix -- for rocprofv3 --pmc
@@ -57,7 +59,7 @@ def parse():
     ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
     ap.add_argument("--workload", default="gpt2-small",
                     choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp",
-                             "kernels"])
+                             "gossip", "kernels"])
     return ap.parse_args()
 
 
@@ -361,6 +363,81 @@ def bench_mlp(args, torch, LU, S):
     m.close()
 
 
+def bench_gossip(args, torch, LU, S):
+    """M = 4 GPT-2-small replicas resident on one GPU take layer-wise steps in
+    turn (worker s mod 4 at step s), each on its own token batch; every unit's
+    locally updated layer is pushed into a receiver drawn per step (seed 4)
+    with the push-sum alpha (Algorithm 1 as written; section 3.1 weights).
+    The replicas share one pair of streams and one workspace.  Reports ms per
+    step and the model disagreement sum((p_updated - q)^2) over all units."""
+    cfg = S.GPT2_SMALL
+    M = 4
+    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch, cfg.vocab)
+    streams = (torch.cuda.Stream(), torch.cuda.Stream())
+    models, ws = [], None
+    gen = torch.Generator(device="cuda")
+    for k in range(M):
+        mk = LU.Model(lc, "adamw", streams=streams, workspace=ws, trace_capacity=16)
+        ws = mk.workspace
+        models.append(mk)
+    gen.manual_seed(1)
+    for t in models[0].infos:
+        view = models[0].params[t["offset"]: t["offset"] + t["numel"]]
+        if t["cols"] > 1:
+            view.normal_(0.0, 0.02, generator=gen)
+        elif t["name"].endswith(".g"):
+            view.fill_(1.0)
+    for k in range(1, M):
+        gen.manual_seed(2 + 100 * k)
+        models[k].params.copy_(models[0].params)
+        noise = torch.empty_like(models[k].params).normal_(0.0, 1e-3, generator=gen)
+        for t in models[k].infos:
+            o = t["offset"]
+            models[k].params[o: o + t["numel"]] += noise[o: o + t["numel"]]
+        del noise
+    torch.cuda.synchronize()
+    for mk in models:
+        LU.layup_refresh_shadow(mk.ctx)
+        mk.synchronize()
+    tokens = [torch.from_numpy(S.gpt_tokens(cfg, seed=10 + k)).cuda() for k in range(M)]
+    pairs = S.gossip_pairs(args.warmup + args.steps, M)
+    w = np.full(M, 1.0 / M)
+    t_own = [0] * M
+    U = models[0].n_units
+    dis = torch.zeros((len(pairs), U), dtype=torch.float32, device="cuda")
+
+    def step(s):
+        i, j = pairs[s]
+        t_own[i] += 1
+        hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, t_own[i])
+        alpha = LU.layup_push_sum_send(w, i, j)
+        LU.layup_step_ex(models[i].ctx, tokens[i], None, hp, alpha, mix_mode=LU.LAYUP_MIX_PUSH,
+                         push_params=models[j].params, push_params_bf16=models[j].params_bf16,
+                         disagreement=dis[s])
+        LU.layup_push_sum_receive(w, i, j)
+
+    for s_ in range(args.warmup):
+        step(s_)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(streams[0])
+    for s_ in range(args.warmup, args.warmup + args.steps):
+        step(s_)
+    e1.record(streams[0])
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    d = dis.sum(dim=1).cpu().numpy()
+    print(json.dumps({"metric": "ms per layer-wise step, 4 resident replicas in push mode",
+                      "workload": "gossip-gpt2-small-x4", "value": round(ms, 3), "unit": "ms/step",
+                      "steps": args.steps, "warmup": args.warmup,
+                      "tokens_per_s": round(cfg.batch * cfg.seq / (ms * 1e-3), 1),
+                      "disagreement_first_last": [float(d[0]), float(d[-1])],
+                      "push_sum_weights": [round(float(x), 6) for x in w], "weight_sum": float(w.sum()),
+                      "data": "synthetic (device-seeded replicas, per-worker token batches)"}), flush=True)
+    for mk in models:
+        mk.close()
+
+
 def bench_kernels(args, torch, LU, S):
     """Single launches for hardware-counter runs, in this order: a 1 GiB
     device copy (known traffic: 1 GiB read + 1 GiB written), the 8 backward
@@ -419,6 +496,8 @@ def main():
             bench_kernels(args, torch, LU, S)
         elif args.workload == "mlp":
             bench_mlp(args, torch, LU, S)
+        elif args.workload == "gossip":
+            bench_gossip(args, torch, LU, S)
         else:
             bench_gpt_other(args, torch, LU, S, args.workload)
         return
@@ -459,6 +538,26 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     loss_v = float(loss.item())
+
+    # drift (section 3.2): delay from each unit's gradient to its applied
+    # update, layer-wise (the last timed step) against one step with every
+    # update after the whole backward pass; model D = beta T (U + 1) / 2
+    drift = {}
+    for name, sched in (("layerwise", LU.LAYUP_SCHEDULE_LAYERWISE),
+                        ("after_backward", LU.LAYUP_SCHEDULE_AFTER_BACKWARD)):
+        if sched == LU.LAYUP_SCHEDULE_AFTER_BACKWARD:
+            step += 1
+            hp.step = step
+            LU.layup_step_ex(model.ctx, td, None, hp, cfg.alpha, schedule=sched, loss_out=loss)
+        f_ms, ready, applied = LU.layup_unit_timeline(model.ctx, model.n_units)
+        delays = [a - r for a, r in zip(applied, ready)]
+        drift[name] = dict(D_ms=round(sum(delays), 4), max_unit_delay_ms=round(max(delays), 4),
+                           step_ms=round(max(applied), 4))
+        if name == "layerwise":
+            bwd = max(ready) - f_ms
+    U = model.n_units
+    drift["backward_ms"] = round(bwd, 4)
+    drift["model_after_backward_D_ms"] = round(bwd * (U + 1) / 2, 4)
 
     # forward pass alone (saved activations + loss gradient), compute stream
     f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -549,6 +648,7 @@ def main():
         "serialized_ms_per_step": round(serial_ms, 4),
         "update_mix_all_units_ms": round(um_all["round_ms"], 4),
         "overlap": round(overlap, 3),
+        "drift": drift,
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

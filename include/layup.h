@@ -275,15 +275,17 @@ layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x,
                         const layup_hparams* hp, float alpha, int32_t peer_slot, float* loss_out,
                         float* disagreement /* device [n_units] or NULL */);
 
-/* Timeline of the last completed step of the context (waits for it): for
- * every unit, the time from the start of the step's forward pass until the
- * unit's gradient was ready (end of its backward on the compute stream) and
- * until its update+mix had been applied (end of the launch on the update
- * stream), in milliseconds, from HIP events.  applied - ready is the delay
- * with which the unit's update lands, the staleness that the drift model of
- * section 3.2 counts.  Host arrays of n_units floats.  LAYUP_ERR_STATE if no
- * whole step has run. */
-layup_status layup_unit_timeline(layup_ctx* ctx, float* ready_ms, float* applied_ms);
+/* Timeline of the last completed step of the context (waits for it), in
+ * milliseconds from the start of the step's forward pass, from HIP events:
+ * forward_ms (host float, nullable) when the forward pass and loss gradient
+ * ended; for every unit, ready_ms when its gradient was ready (end of its
+ * backward on the compute stream) and applied_ms when its update+mix had
+ * been applied (end of the launch on the update stream).  applied - ready is
+ * the delay with which the unit's update lands, the drift that section 3.2
+ * counts per layer; the last ready time minus forward_ms is the backward
+ * time.  ready_ms and applied_ms are host arrays of n_units floats.
+ * LAYUP_ERR_STATE if no whole step has run. */
+layup_status layup_unit_timeline(layup_ctx* ctx, float* forward_ms, float* ready_ms, float* applied_ms);
 
 /* ------------------------------------------------------------- push-sum */
 

@@ -143,6 +143,7 @@ struct layup_ctx {
   std::vector<hipEvent_t> ev_unit;     // gradient of unit u ready (compute stream)
   std::vector<hipEvent_t> ev_applied;  // update+mix of unit u done (update stream)
   hipEvent_t ev_start = nullptr;       // start of the step's forward pass
+  hipEvent_t ev_fwd_end = nullptr;     // end of the forward pass (loss gradient formed)
   hipEvent_t ev_join = nullptr;
   bool timeline_valid = false;
   bool have_join = false;
@@ -694,7 +695,7 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
       return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
     }
   }
-  if (hipEventCreate(&c->ev_start) != hipSuccess ||
+  if (hipEventCreate(&c->ev_start) != hipSuccess || hipEventCreate(&c->ev_fwd_end) != hipSuccess ||
       hipEventCreateWithFlags(&c->ev_join, hipEventDisableTiming) != hipSuccess) {
     layup_destroy(c);
     return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
@@ -710,6 +711,7 @@ void layup_destroy(layup_ctx* ctx) {
   for (auto e : ctx->ev_applied)
     if (e) hipEventDestroy(e);
   if (ctx->ev_start) hipEventDestroy(ctx->ev_start);
+  if (ctx->ev_fwd_end) hipEventDestroy(ctx->ev_fwd_end);
   if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
   delete ctx;
 }
@@ -744,6 +746,7 @@ layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x
   layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_forward(ctx, tokens, loss_out)
                                                             : mlp_forward(ctx, tokens, x, loss_out);
   if (st != LAYUP_OK) return st;
+  HIPCHK(ctx, hipEventRecord(ctx->ev_fwd_end, ctx->sc), "record forward end");
   ctx->forward_done = true;
   ctx->next_backward = ctx->L.n_units - 1;
   return LAYUP_OK;
@@ -888,10 +891,11 @@ layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x, c
   return layup_step_ex(ctx, &a);
 }
 
-layup_status layup_unit_timeline(layup_ctx* ctx, float* ready_ms, float* applied_ms) {
+layup_status layup_unit_timeline(layup_ctx* ctx, float* forward_ms, float* ready_ms, float* applied_ms) {
   if (!ctx || !ready_ms || !applied_ms) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null argument");
   if (!ctx->timeline_valid) return fail(ctx, LAYUP_ERR_STATE, "no whole step has run since the last forward");
   TRY(layup_synchronize(ctx));
+  if (forward_ms) HIPCHK(ctx, hipEventElapsedTime(forward_ms, ctx->ev_start, ctx->ev_fwd_end), "forward time");
   for (int u = 0; u < ctx->L.n_units; ++u) {
     HIPCHK(ctx, hipEventElapsedTime(&ready_ms[u], ctx->ev_start, ctx->ev_unit[u]), "unit ready time");
     HIPCHK(ctx, hipEventElapsedTime(&applied_ms[u], ctx->ev_start, ctx->ev_applied[u]), "unit applied time");

@@ -120,7 +120,7 @@ def lib() -> C.CDLL:
         "layup_unit_update_push": ([P, C.c_int32, P, C.c_float, P, P, P], C.c_int),
         "layup_step_ex": ([P, P], C.c_int),
         "layup_step": ([P, P, P, P, C.c_float, C.c_int32, P, P], C.c_int),
-        "layup_unit_timeline": ([P, P, P], C.c_int),
+        "layup_unit_timeline": ([P, P, P, P], C.c_int),
         "layup_push_sum_send": ([P, C.c_int32, C.c_int32, C.c_int32, P], C.c_int),
         "layup_push_sum_receive": ([P, C.c_int32, C.c_int32, C.c_int32], C.c_int),
         "layup_activation": ([P, C.c_int32, C.c_int32, P, P, P], C.c_int),
@@ -276,10 +276,10 @@ def layup_step_ex(ctx, tokens, x, hp: layup_hparams, alpha: float, schedule: int
 
 
 def layup_unit_timeline(ctx, n_units: int):
-    """(ready_ms, applied_ms) lists of the last whole step."""
-    r, a = (C.c_float * n_units)(), (C.c_float * n_units)()
-    _check(lib().layup_unit_timeline(ctx, r, a), ctx)
-    return list(r), list(a)
+    """(forward_ms, ready_ms list, applied_ms list) of the last whole step."""
+    f, r, a = C.c_float(), (C.c_float * n_units)(), (C.c_float * n_units)()
+    _check(lib().layup_unit_timeline(ctx, C.byref(f), r, a), ctx)
+    return f.value, list(r), list(a)
 
 
 def layup_push_sum_send(w, sender: int, receiver: int) -> float:

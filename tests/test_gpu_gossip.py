@@ -247,7 +247,8 @@ def test_after_backward_schedule_equals_layerwise_and_lands_later():
         for step in (1, 2):
             hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, step)
             LU.layup_step_ex(m.ctx, tokens, None, hp, cfg.alpha, schedule=sched, disagreement=dis)
-        ready, applied = LU.layup_unit_timeline(m.ctx, m.n_units)
+        fwd, ready, applied = LU.layup_unit_timeline(m.ctx, m.n_units)
+        assert 0 < fwd < min(ready)
         out[sched] = dict(p=m.params.cpu().numpy(), mo=m.m.cpu().numpy(), v=m.v.cpu().numpy(),
                           g=m.grads.cpu().numpy(), dis=dis.cpu().numpy(), trace=m.read_trace(),
                           ready=ready, applied=applied)
