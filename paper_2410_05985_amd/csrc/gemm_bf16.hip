@@ -4,30 +4,31 @@
 // (LayUp Algorithm 1, "Backward pass at layer l"), plus the forward and the
 // attention products that produce what the backward reads.
 //
-// Structure: 256 threads = 4 wave64s in a 2x2 grid; a BM x BN block tile,
-// each wave a (BM/2) x (BN/2) tile of 32x32 MFMA blocks.  K advances in
-// steps of 64 through double-buffered LDS (one barrier per step); the next
-// step's global loads are in flight while the current step's MFMAs run.
-// Operands land in LDS k-contiguous ([row][k], padded rows) whatever their
-// layout in HBM: a k-contiguous operand is copied with 128-bit loads/stores;
-// an m/n-contiguous operand (the transposed operands of dW = dY^T X) is
-// loaded as 4(k) x 8(m) blocks with 128-bit loads and transposed in
-// registers before 64-bit LDS stores.  Each lane then reads its 8 k-values
-// of an MFMA operand with one 128-bit LDS read.
+// Structure: a BM x BN block tile computed by a WGM x WGN grid of wave64s,
+// each wave a (BM/WGM) x (BN/WGN) tile of 32x32 MFMA blocks with float32
+// accumulators in registers.  K advances in steps of 32 through a ring of LDS
+// stages filled by direct-to-LDS loads (see the pipeline notes below), so
+// several K steps of both operands are in flight while one is multiplied and
+// no registers stage the copy.  An operand that is k-contiguous in HBM stays
+// k-contiguous in LDS and is read with 128-bit LDS reads; an m/n-contiguous
+// operand (the transposed operands of dW = dY^T X) stays m-contiguous and is
+// read with the transposing LDS read (ds_read_b64_tr_b16), so neither layout
+// is transposed in registers.
 //
-// Block tiles are remapped so that consecutive tiles of one output row band
-// run on the same XCD (workgroups are dealt round-robin over the 8 XCDs,
-// each with its own L2), then grouped along M for L2 reuse of B.
-// Split-K (float32 partials + fixed-order reduction, deterministic) is used
-// when the output has too few tiles to fill 256 CUs.
+// The grid is one flat list of (batch or split, tile) work items dealt out
+// XCD-aware: workgroups are dispatched round-robin over the 8 XCDs (each with
+// its own L2), so consecutive work items are mapped onto one XCD and tiles
+// sharing an operand band hit the same L2.  Split-K (float32 partials + a
+// fixed-order reduction, deterministic) fills the 256 CUs when the output has
+// too few tiles.  Causal attention products skip the tiles and K ranges that
+// the mask makes zero.  Epilogues fuse bias, residual add, GELU (storing the
+// pre-activation and the activation) and the GELU backward.
 #include "layup_internal.h"
 
 namespace layup {
 
 namespace {
 
-constexpr int BK = 64;          // K step per LDS stage
-constexpr int THREADS = 256;    // 4 wave64s in a 2x2 grid
 
 struct KArgs {
   const bf16_t* A;
