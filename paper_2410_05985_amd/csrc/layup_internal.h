@@ -80,7 +80,7 @@ enum Causal : int { CAUSAL_NONE = 0, CAUSAL_OUT_LOWER = 1, CAUSAL_A_LOWER = 2, C
 // Validates shapes/alignment; returns a message or empty string.
 std::string gemm_check(const Gemm& g, bool f32_operands);
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t stream);
-// explicit tile configuration (0 = 256x256, 1 = 256x128, 2 = 128x256, 3 = 128x128, 4 = 128x64)
+// explicit tile configuration (0 = 256x256, 1 = 128x128 with 8 waves, 2 = 128x64, 3 = 128x128 with 4 waves)
 hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t stream);
 hipError_t launch_gemm_f32(const Gemm& g, hipStream_t stream);
 
@@ -100,6 +100,14 @@ hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, f
                               hipStream_t s);
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
                               float scale, hipStream_t s);
+// Fused causal attention (head width 32, 64 or 128): P, O (bf16) and the
+// float32 O from qkv; dS and dQ from qkv, P, dO and the float32 O.
+bool attention_fused_supported(int dh);
+hipError_t launch_attention_fwd(const bf16_t* qkv, bf16_t* P, bf16_t* O, float* Of, int B, int H,
+                                int T, int dh, float scale, hipStream_t s);
+hipError_t launch_attention_bwd(const bf16_t* qkv, const bf16_t* P, const bf16_t* dO, const float* Of,
+                                bf16_t* dS, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
+                                hipStream_t s);
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B,
                              int T, int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
                              hipStream_t s);

@@ -131,7 +131,14 @@ struct Carver {
 struct BlockActs {
   float *x, *h, *mean1, *rstd1, *mean2, *rstd2;
   bf16_t *a, *qkv, *P, *o, *a2, *f, *gl;
+  float* of;  // float32 attention output (fused attention: rowsum(dP P) = dO . O)
 };
+
+// Fused attention kernels cover head widths 32, 64 and 128; other widths use
+// the score GEMM + softmax + GEMM kernels.
+bool fused_attention(const layup_config& g) {
+  return g.model == LAYUP_MODEL_GPT_BF16 && attention_fused_supported(g.d_model / g.n_head);
+}
 
 }  // namespace
 
@@ -190,6 +197,7 @@ size_t carve(layup_ctx* c, char* base) {
   if (g.model == LAYUP_MODEL_GPT_BF16) {
     const int64_t N = (int64_t)g.batch * g.seq, d = g.d_model, F = g.d_ff, H = g.n_head, T = g.seq;
     const int64_t Vp = align64(g.vocab);
+    const bool fused = fused_attention(g);
     c->acts.assign(g.n_layer, BlockActs{});
     for (int l = 0; l < g.n_layer; ++l) {
       BlockActs& A = c->acts[l];
@@ -206,6 +214,7 @@ size_t carve(layup_ctx* c, char* base) {
       A.a2 = cv.take<bf16_t>(N * d);
       A.f = cv.take<bf16_t>(N * F);
       A.gl = cv.take<bf16_t>(N * F);
+      A.of = fused ? cv.take<float>(N * d) : nullptr;
     }
     c->xL = cv.take<float>(N * d);
     c->meanf = cv.take<float>(N);
@@ -214,7 +223,7 @@ size_t carve(layup_ctx* c, char* base) {
     c->logits = cv.take<bf16_t>(N * Vp);
     c->loss_rows = cv.take<float>(N);
     c->sorted = cv.take<uint32_t>(N);
-    c->S = cv.take<float>(g.batch * H * T * T);
+    c->S = fused ? nullptr : cv.take<float>(g.batch * H * T * T);
     c->dS = cv.take<bf16_t>(g.batch * H * T * T);
     c->dx[0] = cv.take<float>(N * d);
     c->dx[1] = cv.take<float>(N * d);
@@ -328,6 +337,10 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
     Gemm q = mk(true, true, N, 3 * d, d, A.a, d, fl.w16(p + "qkv.w"), d, A.qkv, 3 * d, EPI_BF16);
     q.bias = fl.p(p + "qkv.b");
     TRY(run_gemm(c, q, s, "qkv forward"));
+    if (A.of) {
+      HIPCHK(c, launch_attention_fwd(A.qkv, A.P, A.o, A.of, (int)B, (int)H, (int)T, (int)dh, scale, s),
+             "attention");
+    } else {
     // scores S[z] = Q_h K_h^T, z = b*H + h
     Gemm sg = mk(true, true, T, T, dh, A.qkv, 3 * d, A.qkv + d, 3 * d, c->S, T, EPI_F32);
     sg.batch = (int)(B * H);
@@ -351,6 +364,7 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
     pv.c_inner = dh;
     pv.causal = CAUSAL_A_LOWER;
     TRY(run_gemm(c, pv, s, "attention output"));
+    }
     Gemm pr = mk(true, true, N, d, d, A.o, d, fl.w16(p + "proj.w"), d, A.h, d, EPI_F32);
     pr.bias = fl.p(p + "proj.b");
     pr.aux = A.x;
@@ -443,16 +457,24 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     return gm;
   };
   const int64_t TT = T * T;
+  if (!A.of) {
   // dP = dO_h V_h^T
   TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
                           T * d, dh, T * 3 * d, dh, H * TT, TT, CAUSAL_OUT_LOWER), s, "dP"));
+  }
   // dV_h = P^T dO_h
   TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
                              EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dV"));
+  if (A.of) {
+    // dS and dQ_h = dS K_h in one pass (dP stays in registers)
+    HIPCHK(c, launch_attention_bwd(A.qkv, A.P, c->do16, A.of, c->dS, c->dqkv16, (int)B, (int)H, (int)T,
+                                   (int)dh, scale, s), "attention backward");
+  } else {
   HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
   // dQ_h = dS K_h
   TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
                              EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_LOWER), s, "dQ"));
+  }
   // dK_h = dS^T Q_h
   TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
                              EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
@@ -682,6 +704,18 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
     return fail(nullptr, LAYUP_ERR_INVALID_ARG, "workspace smaller than layup_workspace_size");
   }
   c->ws_bytes = carve(c, (char*)workspace);
+  if (cfg->model == LAYUP_MODEL_GPT_BF16) {
+    // probabilities and score gradients above the diagonal are zero and no
+    // kernel writes them: clear both matrices once
+    const size_t pm = (size_t)cfg->batch * cfg->n_head * cfg->seq * cfg->seq * sizeof(bf16_t);
+    bool ok = true;
+    for (auto& A : c->acts) ok = ok && hipMemsetAsync(A.P, 0, pm, (hipStream_t)compute_stream) == hipSuccess;
+    ok = ok && hipMemsetAsync(c->dS, 0, pm, (hipStream_t)compute_stream) == hipSuccess;
+    if (!ok) {
+      delete c;
+      return fail(nullptr, LAYUP_ERR_HIP, "clearing the attention matrices failed");
+    }
+  }
   c->sc = (hipStream_t)compute_stream;
   c->su = update_stream ? (hipStream_t)update_stream : c->sc;
   hipGetDevice(&c->device);

@@ -96,6 +96,12 @@ GPT_TEST = GPTConfig(n_layer=2, d_model=128, n_head=2, d_ff=512, seq=128, batch=
                      vocab=1000, name="gpt-test")
 GPT_TEST_RAGGED = GPTConfig(n_layer=2, d_model=96, n_head=3, d_ff=384, seq=80,
                             batch=3, vocab=517, name="gpt-test-ragged")
+# Head width 128 (as in the 1.3B stack) with a ragged sequence, and head width
+# 48, which the fused attention kernels do not cover (score GEMM + softmax).
+GPT_TEST_DH128 = GPTConfig(n_layer=1, d_model=256, n_head=2, d_ff=512, seq=96, batch=2,
+                           vocab=300, name="gpt-test-dh128")
+GPT_TEST_DH48 = GPTConfig(n_layer=1, d_model=96, n_head=2, d_ff=256, seq=64, batch=2,
+                          vocab=200, name="gpt-test-dh48")
 
 RESNET50_UPDATE = dict(lr=0.1, momentum=0.9, weight_decay=5e-5, alpha=0.5)
 

@@ -120,7 +120,8 @@ def check_adamw_params(got, ref, g_ref, lr, alpha, name):
                       + 1e-5 * (np.abs(ref[loose]) + 1e-3)), name
 
 
-@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48],
+                         ids=lambda c: c.name)
 def test_gpt_forward_activations(cfg):
     """Saved forward activations against the oracle's forward (bf16 storage
     points on both sides; chained)."""
@@ -151,7 +152,8 @@ def test_gpt_forward_activations(cfg):
     m.close()
 
 
-@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48],
+                         ids=lambda c: c.name)
 def test_gpt_step_parity(cfg):
     """One layer-wise step, chained: every gradient at rel 2e-2 (bf16 GEMM
     operands, float32 accumulation), AdamW moments and the mixed parameters as
