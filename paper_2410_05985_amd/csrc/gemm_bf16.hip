@@ -328,30 +328,35 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   }
 }
 
-// Fixed-order sum of split-K partials plus the epilogue.
+// Fixed-order sum of split-K partials plus the float32 epilogue (bias,
+// residual).  Grid: x = 1024-column chunk, y = row; each thread sums four
+// consecutive columns, with 128-bit accesses when N and ldc are multiples of
+// 4 and every pointer is 16-byte aligned.
 template <int EPI>
-__global__ void splitk_reduce_kernel(const KArgs P) {
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
+  static_assert(EPI == EPI_F32, "split-K is used with the float32 epilogue only");
+  const int64_t m = blockIdx.y;
+  const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (n >= P.N) return;
   const int64_t total = P.M * P.N;
-  for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t m = idx / P.N, n = idx % P.N;
-    float v = 0.f;
-    for (int s = 0; s < P.splits; ++s) v += P.partial[(int64_t)s * total + idx];
-    const int64_t off = m * P.ldc + n;
-    float bn = P.bias ? P.bias[n] : 0.f;
-    if (EPI == EPI_F32) {
-      v += bn;
-      if (P.aux) v += reinterpret_cast<const float*>(P.aux)[off];
-      reinterpret_cast<float*>(P.C)[off] = v;
-    } else if (EPI == EPI_BF16) {
-      reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v + bn);
-    } else if (EPI == EPI_GELU) {
-      v += bn;
-      reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v);
-      reinterpret_cast<bf16_t*>(P.C2)[off] = f2bf(gelu_tanh_f(v));
-    } else {
-      float f = bf2f(reinterpret_cast<const bf16_t*>(P.aux)[off]);
-      reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v * gelu_tanh_grad_f(f));
+  const float* src = P.partial + m * P.N + n;
+  float* dst = reinterpret_cast<float*>(P.C) + m * P.ldc + n;
+  const float* aux = P.aux ? reinterpret_cast<const float*>(P.aux) + m * P.ldc + n : nullptr;
+  const bool vec = ((P.N | P.ldc) & 3) == 0 &&
+                   (((uintptr_t)P.C | (uintptr_t)P.aux | (uintptr_t)P.bias | (uintptr_t)P.partial) & 15) == 0;
+  if (vec) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(src);
+    for (int s = 1; s < P.splits; ++s) v += *reinterpret_cast<const f32x4*>(src + s * total);
+    if (P.bias) v += *reinterpret_cast<const f32x4*>(P.bias + n);
+    if (aux) v += *reinterpret_cast<const f32x4*>(aux);
+    *reinterpret_cast<f32x4*>(dst) = v;
+  } else {
+    for (int e = 0; e < 4 && n + e < P.N; ++e) {
+      float v = src[e];
+      for (int s = 1; s < P.splits; ++s) v += src[s * total + e];
+      if (P.bias) v += P.bias[n + e];
+      if (aux) v += aux[e];
+      dst[e] = v;
     }
   }
 }
@@ -367,9 +372,8 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
       gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      int64_t total = P.M * P.N;
-      int blocks = (int)std::min<int64_t>(cdiv(total, 256), 4096);
-      splitk_reduce_kernel<EPI><<<blocks, 256, 0, s>>>(P);
+      const dim3 rgrid((unsigned)cdiv(P.N, 1024), (unsigned)P.M);
+      splitk_reduce_kernel<EPI><<<rgrid, 256, 0, s>>>(P);
       return hipGetLastError();
     }
   }
@@ -467,7 +471,7 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
   const int BM = kShapes[cfg].bm, BN = kShapes[cfg].bn;
   P.tiles_m = (int)cdiv(g.M, BM);
   P.tiles_n = (int)cdiv(g.N, BN);
-  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32) {
+  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32 && g.M <= 65535) {
     while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
     if (splits > 1) {
       P.k_per_split = cdiv(cdiv(g.K, splits), 32) * 32;

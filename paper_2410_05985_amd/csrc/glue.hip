@@ -176,7 +176,7 @@ constexpr int LN_MAXV = 8;  // float4 groups per lane: d <= 2048
 __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, const float* x,
                                                             const float* mean, const float* rstd,
                                                             const float* g, const float* dres,
-                                                            float* dx, float* pg, float* pb,
+                                                            float* dx, bf16_t* dx16, float* part,
                                                             int64_t rows, int d) {
   extern __shared__ f32x4 ln_red[];  // [2][4][nv]
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -223,6 +223,7 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, con
         o[e] += r * (a[e] * gg[e] - s1 - xh * s2);
       }
       reinterpret_cast<f32x4*>(dx + row * d)[i] = o;
+      if (dx16) reinterpret_cast<u32x2*>(dx16 + row * d)[i] = u32x2{pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3])};
     }
   }
 #pragma unroll
@@ -240,32 +241,37 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, con
       sg += red_g[k * nv + i];
       sb += red_b[k * nv + i];
     }
-    reinterpret_cast<f32x4*>(pg + (int64_t)blockIdx.x * d)[i] = sg;
-    reinterpret_cast<f32x4*>(pb + (int64_t)blockIdx.x * d)[i] = sb;
+    // partial row of this block: [dg (d) | db (d)]
+    reinterpret_cast<f32x4*>(part + (int64_t)blockIdx.x * 2 * d)[i] = sg;
+    reinterpret_cast<f32x4*>(part + (int64_t)blockIdx.x * 2 * d + d)[i] = sb;
   }
 }
 
+template <typename T>
+hipError_t colsum2(const T* x, int64_t rows, int64_t cols, int64_t ld, const ColsumScratch& cs,
+                   float* out, float* out2, int64_t split, hipStream_t s);
+
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres, float* dx,
-                                float* pg, float* pb, float* cs_scratch, float* dg, float* db,
-                                int64_t rows, int d, hipStream_t s) {
+                                bf16_t* dx16, float* part, const ColsumScratch& cs, float* dg,
+                                float* db, int64_t rows, int d, hipStream_t s) {
   if (d / 4 > LN_MAXV * 64) return hipErrorInvalidValue;
   const unsigned nb = (unsigned)cdiv(rows, LN_ROWS);
   const size_t lds = (size_t)2 * 4 * (d / 4) * sizeof(f32x4);
-  layernorm_bwd_kernel<<<nb, 256, lds, s>>>(dy, x, mean, rstd, g, dres, dx, pg, pb, rows, d);
+  layernorm_bwd_kernel<<<nb, 256, lds, s>>>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_colsum_f32(pg, nb, d, d, cs_scratch, dg, s);
-  if (e != hipSuccess) return e;
-  return launch_colsum_f32(pb, nb, d, d, cs_scratch, db, s);
+  // dg and db: one column sum over the [nb][2d] partial rows
+  return colsum2<float>(part, nb, 2 * d, 2 * d, cs, dg, db, d, s);
 }
 
 // ------------------------------------------------------------ column sums
-// out[c] = sum over rows of x[r*ld + c], in a fixed order: stage 1 sums
+// out[c] = sum over rows of x[r*ld + c] in a fixed order: stage 1 sums
 // chunks of CS_ROWS rows (inside a chunk: rows r = l, l+8, ... per row lane
-// l, then the 8 row lanes in order), stage 2 sums the chunk partials in chunk
-// order.  Stage 1 reads 16 bytes per thread per row, coalesced across the
-// 32 column groups of a block.
+// l, then the 8 row lanes in order) into partial rows, stage 2 sums the
+// partial rows in chunk order.  Stage 1 reads 16 bytes per thread per row,
+// coalesced across the 32 column groups of a block.  Columns >= split go to
+// out2[c - split] when out2 is given.
 constexpr int CS_ROWS = 128;
 
 template <typename T>
@@ -318,7 +324,7 @@ __global__ __launch_bounds__(256) void colsum_stage1(const T* x, int64_t rows, i
   }
 }
 
-// Scalar fallback for narrow or unaligned inputs (the float32 MLP's 10 classes).
+// Scalar stage 1 for narrow or unaligned inputs (the float32 MLP's 10 classes).
 template <typename T>
 __global__ void colsum_scalar(const T* x, int64_t rows, int64_t cols, int64_t ld, float* partial) {
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -336,7 +342,8 @@ __global__ void colsum_scalar(const T* x, int64_t rows, int64_t cols, int64_t ld
 // 64 columns x 4 chunk lanes per block: lane l sums chunks l, l+4, ... in
 // order, then the four lane sums are added in lane order.
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial, int64_t chunks,
-                                                           int64_t cols, float* out) {
+                                                           int64_t cols, float* out, float* out2,
+                                                           int64_t split) {
   __shared__ float red[4][64];
   const int cl = threadIdx.x & 63, l = threadIdx.x >> 6;
   const int64_t c = (int64_t)blockIdx.x * 64 + cl;
@@ -345,36 +352,41 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* partial,
     for (int64_t k = l; k < chunks; k += 4) s += partial[k * cols + c];
   red[l][cl] = s;
   __syncthreads();
-  if (l == 0 && c < cols) out[c] = (red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl]);
+  if (l == 0 && c < cols) {
+    const float t = (red[0][cl] + red[1][cl]) + (red[2][cl] + red[3][cl]);
+    if (out2 && c >= split) out2[c - split] = t;
+    else out[c] = t;
+  }
 }
 
 template <typename T>
-hipError_t colsum(const T* x, int64_t rows, int64_t cols, int64_t ld, float* partial, float* out,
-                  hipStream_t s) {
+hipError_t colsum2(const T* x, int64_t rows, int64_t cols, int64_t ld, const ColsumScratch& cs,
+                   float* out, float* out2, int64_t split, hipStream_t s) {
   constexpr int VEC = 16 / sizeof(T);
   const int64_t chunks = cdiv(rows, CS_ROWS);
+  if (chunks > 65535 || chunks * cols > cs.partial_floats) return hipErrorInvalidValue;
   const bool vec = cols % VEC == 0 && ld % VEC == 0 && ((uintptr_t)x & 15) == 0;
   if (vec) {
     dim3 g1((unsigned)cdiv(cols, 32 * VEC), (unsigned)chunks);
-    colsum_stage1<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+    colsum_stage1<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, cs.partial);
   } else {
     dim3 g1((unsigned)cdiv(cols, 256), (unsigned)chunks);
-    colsum_scalar<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, partial);
+    colsum_scalar<T><<<g1, 256, 0, s>>>(x, rows, cols, ld, cs.partial);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  colsum_final_kernel<<<(unsigned)cdiv(cols, 64), 256, 0, s>>>(partial, chunks, cols, out);
+  colsum_final_kernel<<<(unsigned)cdiv(cols, 64), 256, 0, s>>>(cs.partial, chunks, cols, out, out2, split);
   return hipGetLastError();
 }
 
 hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              float* partial, float* out, hipStream_t s) {
-  return colsum<bf16_t>(x, rows, cols, ld, partial, out, s);
+                              const ColsumScratch& cs, float* out, hipStream_t s) {
+  return colsum2<bf16_t>(x, rows, cols, ld, cs, out, nullptr, 0, s);
 }
 
 hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
-                             float* partial, float* out, hipStream_t s) {
-  return colsum<float>(x, rows, cols, ld, partial, out, s);
+                             const ColsumScratch& cs, float* out, hipStream_t s) {
+  return colsum2<float>(x, rows, cols, ld, cs, out, nullptr, 0, s);
 }
 
 // ------------------------------------------------------- causal softmax

@@ -89,13 +89,18 @@ hipError_t launch_embed_fwd(const int32_t* tokens, const float* wte, const float
                             int B, int T, int d, int V, hipStream_t s);
 hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int64_t rows, int d, hipStream_t s);
-// dg/db partial rows go to pg/pb (rows/16 x d each); cs_scratch holds
-// ceil(rows/16/128) x d floats for the final column sums.
+// Scratch of the column sums: partial rows, ceil(rows/128) x cols floats.
+struct ColsumScratch {
+  float* partial;
+  int64_t partial_floats;
+};
+// LayerNorm backward: dx (float32) and optionally its bfloat16 copy dx16;
+// per-16-row partial sums of dg and db go to part (ceil(rows/16) x 2d floats)
+// and are reduced into dg, db.
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres,
-                                float* dx, float* pg, float* pb, float* cs_scratch, float* dg,
-                                float* db, int64_t rows, int d, hipStream_t s);
-// Column sums: partial must hold ceil(rows/128) x cols floats.
+                                float* dx, bf16_t* dx16, float* part, const ColsumScratch& cs,
+                                float* dg, float* db, int64_t rows, int d, hipStream_t s);
 hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
                               hipStream_t s);
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
@@ -113,9 +118,9 @@ hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* to
                              hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s);
 hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              float* partial, float* out, hipStream_t s);
+                              const ColsumScratch& cs, float* out, hipStream_t s);
 hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
-                             float* partial, float* out, hipStream_t s);
+                             const ColsumScratch& cs, float* out, hipStream_t s);
 hipError_t launch_embed_bwd(const float* dx, const int32_t* sorted_pos, float* dwte, float* dwpe,
                             int B, int T, int d, int V, hipStream_t s);
 hipError_t launch_token_sort(const int32_t* tokens, int B, int T, int V, int32_t* counts,

@@ -175,7 +175,9 @@ struct layup_ctx {
   float* dh = nullptr;
   float* da = nullptr;
   bf16_t *dy16 = nullptr, *df16 = nullptr, *do16 = nullptr, *dqkv16 = nullptr;
-  float *ln_pg = nullptr, *ln_pb = nullptr, *cs_part = nullptr;
+  float *ln_part = nullptr, *cs_part = nullptr;
+  int64_t cs_part_floats = 0;
+  ColsumScratch cs() const { return ColsumScratch{cs_part, cs_part_floats}; }
   float* splitk = nullptr;
   size_t splitk_bytes = 0;
   float* dis_partial = nullptr;
@@ -233,9 +235,9 @@ size_t carve(layup_ctx* c, char* base) {
     c->df16 = cv.take<bf16_t>(N * F);
     c->do16 = cv.take<bf16_t>(N * d);
     c->dqkv16 = cv.take<bf16_t>(N * 3 * d);
-    c->ln_pg = cv.take<float>(cdiv(N, 16) * d);
-    c->ln_pb = cv.take<float>(cdiv(N, 16) * d);
-    c->cs_part = cv.take<float>(cdiv(N, 128) * std::max<int64_t>(3 * d, F));
+    c->ln_part = cv.take<float>(cdiv(N, 16) * 2 * d);
+    c->cs_part_floats = cdiv(N, 128) * std::max<int64_t>(3 * d, F);
+    c->cs_part = cv.take<float>(c->cs_part_floats);
     c->splitk = cv.take<float>(SPLITK_BYTES / 4);
     c->splitk_bytes = SPLITK_BYTES;
   } else {
@@ -247,7 +249,8 @@ size_t carve(layup_ctx* c, char* base) {
     c->mlp_dz = cv.take<float>(g.batch * wmax);
     c->mlp_dh = cv.take<float>(g.batch * wmax);
     c->loss_rows = cv.take<float>(g.batch);
-    c->cs_part = cv.take<float>(cdiv(g.batch, 128) * wmax);
+    c->cs_part_floats = cdiv(g.batch, 128) * wmax;
+    c->cs_part = cv.take<float>(c->cs_part_floats);
   }
   c->dis_partial = cv.take<float>(UM_MAX_BLOCKS);
   return cv.used + 256;
@@ -404,7 +407,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     TRY(run_gemm(c, dw, s, "head dW"));
     c->cur_dx = 0;
     HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
-                                   c->dx[0], c->ln_pg, c->ln_pb, c->cs_part, fl.g("lnf.g"), fl.g("lnf.b"), N,
+                                   c->dx[0], c->dy16, c->ln_part, c->cs(), fl.g("lnf.g"), fl.g("lnf.b"), N,
                                    (int)d, s), "lnf backward");
     return LAYUP_OK;
   }
@@ -419,27 +422,27 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   float* dxo = c->dx[c->cur_dx];
   float* dxi = c->dx[c->cur_dx ^ 1];
   // MLP output projection
-  HIPCHK(c, launch_f32_to_bf16(dxo, c->dy16, N * d, s), "dy cast");
+  // c->dy16 holds bf16(dxo), written by the LayerNorm backward that produced dxo
   TRY(run_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32), s,
                "mproj dW"));
-  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs_part, fl.g(p + "mproj.b"), s), "mproj db");
+  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "mproj.b"), s), "mproj db");
   Gemm dg = mk(true, false, N, F, d, c->dy16, d, fl.w16(p + "mproj.w"), F, c->df16, F, EPI_DGELU);
   dg.aux = A.f;
   TRY(run_gemm(c, dg, s, "mproj dX + gelu backward"));
   // MLP input projection
   TRY(run_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32), s,
                "fc dW"));
-  HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs_part, fl.g(p + "fc.b"), s), "fc db");
+  HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs(), fl.g(p + "fc.b"), s), "fc db");
   TRY(run_gemm(c, mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32), s,
                "fc dX"));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
-                                 c->ln_pg, c->ln_pb, c->cs_part, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
+                                 c->dy16, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
   // attention output projection
-  HIPCHK(c, launch_f32_to_bf16(c->dh, c->dy16, N * d, s), "dy2 cast");
+  // c->dy16 now holds bf16(dh) from the LayerNorm backward above
   TRY(run_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32), s,
                "proj dW"));
-  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs_part, fl.g(p + "proj.b"), s), "proj db");
+  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "proj.b"), s), "proj db");
   TRY(run_gemm(c, mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16),
                s, "proj dX"));
   // attention core, batched over z = b*H + h
@@ -481,11 +484,12 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   // qkv projection
   TRY(run_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
                      EPI_F32), s, "qkv dW"));
-  HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs_part, fl.g(p + "qkv.b"), s), "qkv db");
+  HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs(), fl.g(p + "qkv.b"), s), "qkv db");
   TRY(run_gemm(c, mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d,
                      EPI_F32), s, "qkv dX"));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
-                                 c->ln_pg, c->ln_pb, c->cs_part, fl.g(p + "ln1.g"), fl.g(p + "ln1.b"), N, (int)d,
+                                 l > 0 ? c->dy16 : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
+                                 fl.g(p + "ln1.b"), N, (int)d,
                                  s), "ln1 backward");
   c->cur_dx ^= 1;
   return LAYUP_OK;
@@ -527,7 +531,7 @@ layup_status mlp_backward(layup_ctx* c, int u) {
   const float* hin = u == 0 ? c->mlp_x : c->mlp_act[u];
   TRY(mlp_gemm(c, mk(false, false, out, in, Bt, c->mlp_dz, out, hin, in, fl.g(p + "w"), in, EPI_F32),
                "mlp dW"));
-  HIPCHK(c, launch_colsum_f32(c->mlp_dz, Bt, out, out, c->cs_part, fl.g(p + "b"), c->sc), "mlp db");
+  HIPCHK(c, launch_colsum_f32(c->mlp_dz, Bt, out, out, c->cs(), fl.g(p + "b"), c->sc), "mlp db");
   if (u > 0) {
     TRY(mlp_gemm(c, mk(true, false, Bt, in, out, c->mlp_dz, out, fl.p(p + "w"), in, c->mlp_dh, in,
                        EPI_F32), "mlp dX"));
