@@ -176,10 +176,10 @@ __device__ __forceinline__ void barrier_only() {
 // 32x32 MFMA tiles.  More waves issue more direct-to-LDS copies in parallel
 // (the copy rate per CU grows with the number of issuing waves).
 // STAGES LDS stages of (BM + BN) x 32 bf16; OCC workgroups per CU.
-template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool AK, bool BKM, int EPI, bool SPLIT>
+template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool AK, bool BKM, int EPI, bool SPLIT,
+          int BKV = 32>
 __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KArgs P) {
   constexpr int NW = WGM * WGN;
-  constexpr int BKV = 32;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
   constexpr int A_BYTES = BM * BKV * 2, STAGE = (BM + BN) * BKV * 2;
@@ -361,7 +361,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI, int BKV = 32>
 hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   const int64_t n_log = (int64_t)P.tiles_m * P.tiles_n * (P.splits > 1 ? P.splits : batch);
   if (n_log >= (1ll << 31) - 8) return hipErrorInvalidValue;
@@ -369,7 +369,7 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   constexpr int NT = 64 * WGM * WGN;
   if constexpr (EPI == EPI_F32) {
     if (P.splits > 1) {
-      gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true><<<grid, NT, 0, s>>>(P);
+      gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true, BKV><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const dim3 rgrid((unsigned)cdiv(P.N, 1024), (unsigned)P.M);
@@ -377,25 +377,25 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, false><<<grid, NT, 0, s>>>(P);
+  gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, false, BKV><<<grid, NT, 0, s>>>(P);
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WGM, int WGN, int STG, int OCC, int EPI>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, int BKV, int EPI>
 hipError_t dispatch_layout(const Gemm& g, const KArgs& P, hipStream_t s) {
-  if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, true, EPI>(P, g.batch, s);
-  if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, false, EPI>(P, g.batch, s);
-  if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI>(P, g.batch, s);
+  if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, true, EPI, BKV>(P, g.batch, s);
+  if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, false, EPI, BKV>(P, g.batch, s);
+  if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI, BKV>(P, g.batch, s);
   return hipErrorInvalidValue;  // m-major A with k-major B: no caller needs it
 }
 
-template <int BM, int BN, int WGM, int WGN, int STG, int OCC>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, int BKV>
 hipError_t dispatch_epi(const Gemm& g, const KArgs& P, hipStream_t s) {
   switch (g.epi) {
-    case EPI_F32: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_F32>(g, P, s);
-    case EPI_BF16: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_BF16>(g, P, s);
-    case EPI_GELU: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_GELU>(g, P, s);
-    default: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, EPI_DGELU>(g, P, s);
+    case EPI_F32: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_F32>(g, P, s);
+    case EPI_BF16: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_BF16>(g, P, s);
+    case EPI_GELU: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_GELU>(g, P, s);
+    default: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_DGELU>(g, P, s);
   }
 }
 
@@ -451,16 +451,17 @@ std::string gemm_check(const Gemm& g, bool f32_operands) {
   return "";
 }
 
-// Tile configurations: tile, wave grid, LDS stages, workgroups per CU.  The
-// copy rate into LDS grows with the number of waves issuing direct-to-LDS
-// loads, so the configurations trade tile size (operand reuse) against waves
-// per CU.
+// Tile configurations: tile, wave grid, LDS stages, workgroups per CU, K
+// step.  The copy rate into LDS grows with the number of waves issuing
+// direct-to-LDS loads, and each K step costs one wait and one barrier, so
+// the configurations trade tile size (operand reuse) against waves per CU
+// and K-step length.
 struct TileShape { int bm, bn; };
 static const TileShape kShapes[] = {
-    {256, 256},  // 0: 4x2 waves (each 64x128), 4 stages, 1/CU  (8 waves/CU)
-    {128, 128},  // 1: 2x4 waves (each 64x32),  3 stages, 3/CU  (24 waves/CU)
-    {128, 64},   // 2: 2x2 waves (each 64x32),  4 stages, 3/CU  (12 waves/CU)
-    {128, 128},  // 3: 2x2 waves (each 64x64),  4 stages, 2/CU  (8 waves/CU)
+    {256, 256},  // 0: 4x2 waves (each 64x128), 2 stages of K 64, 1/CU  (8 waves/CU)
+    {128, 128},  // 1: 2x4 waves (each 64x32),  3 stages of K 32, 3/CU  (24 waves/CU)
+    {128, 64},   // 2: 2x2 waves (each 64x32),  4 stages of K 32, 3/CU  (12 waves/CU)
+    {128, 128},  // 3: 2x4 waves (each 64x32),  2 stages of K 64, 2/CU  (16 waves/CU)
 };
 constexpr int kNumCfg = 4;
 
@@ -480,41 +481,42 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
     }
   }
   switch (cfg) {
-    case 0: return dispatch_epi<256, 256, 4, 2, 4, 1>(g, P, s);
-    case 1: return dispatch_epi<128, 128, 2, 4, 3, 3>(g, P, s);
-    case 2: return dispatch_epi<128, 64, 2, 2, 4, 3>(g, P, s);
-    default: return dispatch_epi<128, 128, 2, 2, 4, 2>(g, P, s);
+    case 0: return dispatch_epi<256, 256, 4, 2, 2, 1, 64>(g, P, s);
+    case 1: return dispatch_epi<128, 128, 2, 4, 3, 3, 32>(g, P, s);
+    case 2: return dispatch_epi<128, 64, 2, 2, 4, 3, 32>(g, P, s);
+    default: return dispatch_epi<128, 128, 2, 4, 2, 2, 64>(g, P, s);
   }
 }
 
-// Tile choice (measured on MI355X over the GPT-2-small/medium/1.3B shapes):
-// 256x256 with 8 waves when both output dimensions and K are large; the
-// 8-wave 128x128 tile elsewhere; 128x64 when N <= 64 (attention head width).
-// Split-K (float32 partials, fixed-order sum) when K >= 1536 and the output
-// has too few tiles to occupy every CU (fewer than 256 tiles of 256x256, or
-// 512 of 128x128).
+// Tile choice, measured inside the GPT-2-small step (operands arriving from
+// HBM, not repeated launches on cached operands):
+//  - N <= 64 (attention head width): 128x64;
+//  - both output dimensions >= 2048, K >= 4096 and at least 256 tiles:
+//    256x256 with K steps of 64;
+//  - float32 dX = dY W (k-major A, m-major B) and dW = dY^T X with fewer than
+//    128 tiles: 128x128 with K steps of 64 (fewer waits and barriers);
+//    split-K when the output has fewer than 300 tiles;
+//  - otherwise (forward products, bf16/GELU epilogues, larger dW): 128x128
+//    with K steps of 32 and three stages (more loads in flight for short K);
+//    split-K for float32 outputs with fewer than 512 tiles (dW: 4 splits).
+// Split-K (float32 partials, fixed-order sum) only with K >= 1536, at least
+// 512 K per split, at most 8 splits.
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
   auto tiles = [&](int bm, int bn) { return cdiv(g.M, bm) * cdiv(g.N, bn) * g.batch; };
-  int cfg;
-  int64_t t;
-  if (g.N <= 64) {
-    cfg = 2;
-    t = tiles(128, 64);
-  } else if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256) {
-    cfg = 0;
-    t = tiles(256, 256);
-  } else {
-    cfg = 1;
-    t = tiles(128, 128);
-  }
-  // workgroups that keep every CU busy: one 256x256 tile or three 128x128
-  // tiles per CU at a time
-  const int64_t want = cfg == 0 ? 256 : 512;
-  int splits = 1;
-  if (g.batch == 1 && t < want && g.K >= 1536)
-    splits = (int)std::min<int64_t>(std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), g.K / 512), 8);
-  return launch_gemm_bf16_cfg(g, cfg, splits, s);
+  const bool splittable = g.batch == 1 && g.K >= 1536 && g.epi == EPI_F32;
+  auto split_for = [&](int64_t t, int64_t want) {
+    if (!splittable || t >= want) return 1;
+    return (int)std::min<int64_t>(std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), g.K / 512), 8);
+  };
+  if (g.N <= 64) return launch_gemm_bf16_cfg(g, 2, 1, s);
+  if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256)
+    return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
+  const int64_t t = tiles(128, 128);
+  if (g.epi == EPI_F32 && !g.b_kmajor && (g.a_kmajor || t < 128))
+    return launch_gemm_bf16_cfg(g, 3, split_for(t, 300), s);
+  if (!g.a_kmajor) return launch_gemm_bf16_cfg(g, 1, splittable && t < 512 ? 4 : 1, s);
+  return launch_gemm_bf16_cfg(g, 1, split_for(t, 512), s);
 }
 
 }  // namespace layup
