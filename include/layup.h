@@ -287,6 +287,17 @@ layup_status layup_step(layup_ctx* ctx, const int32_t* tokens, const float* x,
  * LAYUP_ERR_STATE if no whole step has run. */
 layup_status layup_unit_timeline(layup_ctx* ctx, float* forward_ms, float* ready_ms, float* applied_ms);
 
+/* GEMM timing of the path: with enable != 0, every later backward of a GPT
+ * block brackets each of its linear layers' dX and dW GEMMs (and their
+ * split-K sums) with HIP events on the compute stream; enabling or disabling
+ * waits for the context and resets the counters.  layup_gemm_timing_read
+ * waits for the context and returns the summed GEMM time in milliseconds,
+ * the number of timed GEMMs and their algorithmic FLOPs (2 M N K each).  The
+ * brackets include each launch's dispatch (a few microseconds per GEMM) and
+ * the events slow the step; leave timing off when timing steps. */
+layup_status layup_gemm_timing(layup_ctx* ctx, int32_t enable);
+layup_status layup_gemm_timing_read(layup_ctx* ctx, float* total_ms, int32_t* launches, double* flops);
+
 /* ------------------------------------------------------------- push-sum */
 
 /* Push-sum weights of the workers (section 3.1): each starts at 1/M; a sender

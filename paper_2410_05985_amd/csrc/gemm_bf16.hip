@@ -383,9 +383,12 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
 
 template <int BM, int BN, int WGM, int WGN, int STG, int OCC, int BKV, int EPI>
 hipError_t dispatch_layout(const Gemm& g, const KArgs& P, hipStream_t s) {
-  if (g.a_kmajor && g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, true, EPI, BKV>(P, g.batch, s);
-  if (g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, false, EPI, BKV>(P, g.batch, s);
-  if (!g.a_kmajor && !g.b_kmajor) return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI, BKV>(P, g.batch, s);
+  if (g.a_kmajor && g.b_kmajor)
+    return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, true, EPI, BKV>(P, g.batch, s);
+  if (g.a_kmajor && !g.b_kmajor)
+    return launch_tiles<BM, BN, WGM, WGN, STG, OCC, true, false, EPI, BKV>(P, g.batch, s);
+  if (!g.a_kmajor && !g.b_kmajor)
+    return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI, BKV>(P, g.batch, s);
   return hipErrorInvalidValue;  // m-major A with k-major B: no caller needs it
 }
 

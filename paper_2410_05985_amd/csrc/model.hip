@@ -153,6 +153,11 @@ struct layup_ctx {
   hipEvent_t ev_fwd_end = nullptr;     // end of the forward pass (loss gradient formed)
   hipEvent_t ev_join = nullptr;
   bool timeline_valid = false;
+  // optional timing of the linear layers' backward GEMMs (events around each)
+  bool gemm_timing = false;
+  std::vector<hipEvent_t> gt_events;  // start/stop pairs
+  int gt_used = 0;
+  double gt_flops = 0.0;
   bool have_join = false;
   std::string err;
   int device = 0;
@@ -304,12 +309,30 @@ Gemm mk(bool ak, bool bk, int64_t M, int64_t N, int64_t K, const void* A, int64_
   return g;
 }
 
-layup_status run_gemm(layup_ctx* c, Gemm g, hipStream_t s, const char* what) {
+// timed: one of a block's linear-layer backward GEMMs (dX or dW); with GEMM
+// timing on, HIP events on its stream bracket the launch (and its split-K sum)
+layup_status run_gemm(layup_ctx* c, Gemm g, hipStream_t s, const char* what, bool timed = false) {
   g.splitk_ws = c->splitk;
   g.splitk_ws_bytes = c->splitk_bytes;
   std::string m = gemm_check(g, false);
   if (!m.empty()) return fail(c, LAYUP_ERR_SHAPE, std::string(what) + ": " + m);
+  timed = timed && c->gemm_timing;
+  if (timed) {
+    if ((size_t)c->gt_used + 2 > c->gt_events.size()) {
+      hipEvent_t e[2];
+      if (hipEventCreate(&e[0]) != hipSuccess || hipEventCreate(&e[1]) != hipSuccess)
+        return fail(c, LAYUP_ERR_HIP, "event creation failed");
+      c->gt_events.push_back(e[0]);
+      c->gt_events.push_back(e[1]);
+    }
+    HIPCHK(c, hipEventRecord(c->gt_events[c->gt_used], s), "GEMM timing event");
+  }
   HIPCHK(c, launch_gemm_bf16(g, s), what);
+  if (timed) {
+    HIPCHK(c, hipEventRecord(c->gt_events[c->gt_used + 1], s), "GEMM timing event");
+    c->gt_used += 2;
+    c->gt_flops += 2.0 * (double)g.M * (double)g.N * (double)g.K * g.batch;
+  }
   return LAYUP_OK;
 }
 
@@ -424,27 +447,27 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   // MLP output projection
   // c->dy16 holds bf16(dxo), written by the LayerNorm backward that produced dxo
   TRY(run_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32), s,
-               "mproj dW"));
+               "mproj dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "mproj.b"), s), "mproj db");
   Gemm dg = mk(true, false, N, F, d, c->dy16, d, fl.w16(p + "mproj.w"), F, c->df16, F, EPI_DGELU);
   dg.aux = A.f;
-  TRY(run_gemm(c, dg, s, "mproj dX + gelu backward"));
+  TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
   // MLP input projection
   TRY(run_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32), s,
-               "fc dW"));
+               "fc dW", true));
   HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs(), fl.g(p + "fc.b"), s), "fc db");
   TRY(run_gemm(c, mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32), s,
-               "fc dX"));
+               "fc dX", true));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
                                  c->dy16, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
   // attention output projection
   // c->dy16 now holds bf16(dh) from the LayerNorm backward above
   TRY(run_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32), s,
-               "proj dW"));
+               "proj dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "proj.b"), s), "proj db");
   TRY(run_gemm(c, mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16),
-               s, "proj dX"));
+               s, "proj dX", true));
   // attention core, batched over z = b*H + h
   auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
                      int64_t ci, int causal) {
@@ -483,10 +506,10 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                              EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   // qkv projection
   TRY(run_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
-                     EPI_F32), s, "qkv dW"));
+                     EPI_F32), s, "qkv dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs(), fl.g(p + "qkv.b"), s), "qkv db");
   TRY(run_gemm(c, mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d,
-                     EPI_F32), s, "qkv dX"));
+                     EPI_F32), s, "qkv dX", true));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
                                  l > 0 ? c->dy16 : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
                                  fl.g(p + "ln1.b"), N, (int)d,
@@ -748,6 +771,7 @@ void layup_destroy(layup_ctx* ctx) {
     if (e) hipEventDestroy(e);
   for (auto e : ctx->ev_applied)
     if (e) hipEventDestroy(e);
+  for (auto e : ctx->gt_events) hipEventDestroy(e);
   if (ctx->ev_start) hipEventDestroy(ctx->ev_start);
   if (ctx->ev_fwd_end) hipEventDestroy(ctx->ev_fwd_end);
   if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
@@ -938,6 +962,30 @@ layup_status layup_unit_timeline(layup_ctx* ctx, float* forward_ms, float* ready
     HIPCHK(ctx, hipEventElapsedTime(&ready_ms[u], ctx->ev_start, ctx->ev_unit[u]), "unit ready time");
     HIPCHK(ctx, hipEventElapsedTime(&applied_ms[u], ctx->ev_start, ctx->ev_applied[u]), "unit applied time");
   }
+  return LAYUP_OK;
+}
+
+layup_status layup_gemm_timing(layup_ctx* ctx, int32_t enable) {
+  if (!ctx) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null context");
+  TRY(layup_synchronize(ctx));
+  ctx->gemm_timing = enable != 0;
+  ctx->gt_used = 0;
+  ctx->gt_flops = 0.0;
+  return LAYUP_OK;
+}
+
+layup_status layup_gemm_timing_read(layup_ctx* ctx, float* total_ms, int32_t* launches, double* flops) {
+  if (!ctx || !total_ms || !launches || !flops) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null argument");
+  TRY(layup_synchronize(ctx));
+  float tot = 0.f;
+  for (int i = 0; i < ctx->gt_used; i += 2) {
+    float ms = 0.f;
+    HIPCHK(ctx, hipEventElapsedTime(&ms, ctx->gt_events[i], ctx->gt_events[i + 1]), "GEMM timing");
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = ctx->gt_used / 2;
+  *flops = ctx->gt_flops;
   return LAYUP_OK;
 }
 

@@ -86,7 +86,7 @@ EXPORTS = [
     "layup_destroy", "layup_last_error", "layup_global_error", "layup_synchronize",
     "layup_refresh_shadow", "layup_forward", "layup_layer_backward", "layup_unit_update_mix",
     "layup_layer_update_mix", "layup_unit_update_push", "layup_step_ex", "layup_step",
-    "layup_unit_timeline", "layup_push_sum_send", "layup_push_sum_receive", "layup_activation",
+    "layup_unit_timeline", "layup_gemm_timing", "layup_gemm_timing_read", "layup_push_sum_send", "layup_push_sum_receive", "layup_activation",
     "layup_gemm_bf16", "layup_gemm_f32",
 ]
 
@@ -121,6 +121,8 @@ def lib() -> C.CDLL:
         "layup_step_ex": ([P, P], C.c_int),
         "layup_step": ([P, P, P, P, C.c_float, C.c_int32, P, P], C.c_int),
         "layup_unit_timeline": ([P, P, P, P], C.c_int),
+        "layup_gemm_timing": ([P, C.c_int32], C.c_int),
+        "layup_gemm_timing_read": ([P, P, P, P], C.c_int),
         "layup_push_sum_send": ([P, C.c_int32, C.c_int32, C.c_int32, P], C.c_int),
         "layup_push_sum_receive": ([P, C.c_int32, C.c_int32, C.c_int32], C.c_int),
         "layup_activation": ([P, C.c_int32, C.c_int32, P, P, P], C.c_int),
@@ -280,6 +282,17 @@ def layup_unit_timeline(ctx, n_units: int):
     f, r, a = C.c_float(), (C.c_float * n_units)(), (C.c_float * n_units)()
     _check(lib().layup_unit_timeline(ctx, C.byref(f), r, a), ctx)
     return f.value, list(r), list(a)
+
+
+def layup_gemm_timing(ctx, enable: bool):
+    _check(lib().layup_gemm_timing(ctx, int(enable)), ctx)
+
+
+def layup_gemm_timing_read(ctx):
+    """(total_ms, launches, flops) of the timed backward GEMMs."""
+    ms, n, fl = C.c_float(), C.c_int32(), C.c_double()
+    _check(lib().layup_gemm_timing_read(ctx, C.byref(ms), C.byref(n), C.byref(fl)), ctx)
+    return ms.value, n.value, fl.value
 
 
 def layup_push_sum_send(w, sender: int, receiver: int) -> float:

@@ -287,3 +287,26 @@ def test_gpt2_small_full_size_step_properties():
     pad = m.params[wte["offset"] + wte["numel"]: wte["offset"] + wte["padded_rows"] * wte["cols"]]
     assert pad.numel() == 47 * 768 and torch.count_nonzero(pad).item() == 0
     m.close()
+
+
+def test_gemm_timing_counts_the_block_backward_gemms():
+    """layup_gemm_timing brackets each block's eight linear-layer backward
+    GEMMs (dX and dW of qkv, proj, fc, mproj): count and FLOPs are exact, the
+    time positive; turning it off leaves later steps untimed."""
+    cfg = S.GPT_TEST
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, _ = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    LU.layup_gemm_timing(m.ctx, True)
+    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0)
+    ms, n, flops = LU.layup_gemm_timing_read(m.ctx)
+    Ntok, d, F = cfg.batch * cfg.seq, cfg.d_model, cfg.d_ff
+    per_block = 2 * Ntok * (3 * d * d + d * d + F * d + d * F) * 2   # dX and dW of each linear
+    assert n == 8 * cfg.n_layer
+    assert flops == per_block * cfg.n_layer
+    assert ms > 0
+    LU.layup_gemm_timing(m.ctx, False)
+    hp.step = 2
+    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0)
+    assert LU.layup_gemm_timing_read(m.ctx)[1] == 0
+    m.close()
