@@ -598,6 +598,21 @@ def main():
     serial_ms = s0.elapsed_time(s1) / args.steps
     ser.close()
     del ser
+
+    # the fused schedule: each block's weight matrices updated by their dW GEMM
+    for _ in range(2):
+        step += 1
+        hp.step = step
+        LU.layup_step_ex(model.ctx, td, None, hp, cfg.alpha, schedule=LU.LAYUP_SCHEDULE_FUSED_DW, loss_out=loss)
+    fz0, fz1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    fz0.record(model.compute_stream)
+    for _ in range(args.steps):
+        step += 1
+        hp.step = step
+        LU.layup_step_ex(model.ctx, td, None, hp, cfg.alpha, schedule=LU.LAYUP_SCHEDULE_FUSED_DW, loss_out=loss)
+    fz1.record(model.compute_stream)
+    fz1.synchronize()
+    fused_ms = fz0.elapsed_time(fz1) / args.steps
     print(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step, loss {loss_v:.4f}", file=sys.stderr,
           flush=True)
 
@@ -612,7 +627,7 @@ def main():
     um_all = time_update_mix(torch, LU, model, range(model.n_units), hp, cfg.alpha, args.kernel_reps, ks)
     overlap = (serial_ms - ms_step) / um_all["round_ms"]
     print(f"[bench] step events p10/median/p90 {percentiles(step_ms)}; forward {fwd_ms:.3f} ms; "
-          f"serialized {serial_ms:.3f} ms; update+mix of all {model.n_units} units {um_all['round_ms']:.3f} ms; "
+          f"serialized {serial_ms:.3f} ms; fused dW {fused_ms:.3f} ms; update+mix of all {model.n_units} units {um_all['round_ms']:.3f} ms; "
           f"overlap {overlap:.2f}", file=sys.stderr, flush=True)
     for x in g:
         print(f"[bench] gemm {x['name']:9s} {x['M']}x{x['N']}x{x['K']}: {x['ms']*1e3:8.1f} us "
@@ -658,6 +673,7 @@ def main():
         "step_ms_events": percentiles(step_ms),
         "forward_ms": round(fwd_ms, 4),
         "serialized_ms_per_step": round(serial_ms, 4),
+        "fused_dw_ms_per_step": round(fused_ms, 4),
         "update_mix_all_units_ms": round(um_all["round_ms"], 4),
         "overlap": round(overlap, 3),
         "drift": drift,

@@ -246,7 +246,17 @@ layup_status layup_unit_update_push(layup_ctx* ctx, int32_t unit, const layup_hp
  *                                  the paper compares against).
  * On one worker both produce the same numbers (no unit's backward reads a
  * unit updated before it); they differ in when each update lands. */
-typedef enum { LAYUP_SCHEDULE_LAYERWISE = 0, LAYUP_SCHEDULE_AFTER_BACKWARD = 1 } layup_schedule;
+typedef enum {
+  LAYUP_SCHEDULE_LAYERWISE = 0,
+  LAYUP_SCHEDULE_AFTER_BACKWARD = 1,
+  /* layer-wise, with each GPT block's weight matrices updated and mixed by
+   * their own dW GEMM (its epilogue, or its split-K sum) right after the
+   * block's dX GEMMs have read them: the matrices' gradients are never
+   * written to HBM (grads keeps stale values for them); the block's vectors
+   * and the embedding / final-LayerNorm units take the update+mix kernel as
+   * in the layer-wise schedule.  GPT model, pull form, no disagreement. */
+  LAYUP_SCHEDULE_FUSED_DW = 2
+} layup_schedule;
 
 /* Arguments of layup_step_ex. */
 typedef struct {

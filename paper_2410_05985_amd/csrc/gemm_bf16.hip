@@ -43,6 +43,7 @@ struct KArgs {
   int32_t inner, splits, tiles_m, tiles_n;
   int32_t causal, nz;      // nz: batch count
   int64_t k_per_split;
+  UpdArgs upd;             // EPI_UPDATE
 };
 
 __device__ __forceinline__ float gelu_tanh_f(float x) {
@@ -319,6 +320,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
           v += bn;
           reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v);
           reinterpret_cast<bf16_t*>(P.C2)[off] = f2bf(gelu_tanh_f(v));
+        } else if (EPI == EPI_UPDATE) {
+          apply_update(P.upd, m * P.ldc + n, v);
         } else {  // EPI_DGELU
           float f = bf2f(reinterpret_cast<const bf16_t*>(P.aux)[off]);
           reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v * gelu_tanh_grad_f(f));
@@ -328,18 +331,36 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   }
 }
 
-// Fixed-order sum of split-K partials plus the float32 epilogue (bias,
-// residual).  Grid: x = 1024-column chunk, y = row; each thread sums four
-// consecutive columns, with 128-bit accesses when N and ldc are multiples of
-// 4 and every pointer is 16-byte aligned.
+// Fixed-order sum of split-K partials plus the epilogue: float32 output
+// (bias, residual) or the fused weight update.  Grid: x = 1024-column chunk,
+// y = row; each thread sums four consecutive columns, with 128-bit accesses
+// when N and ldc are multiples of 4 and every pointer is 16-byte aligned.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
-  static_assert(EPI == EPI_F32, "split-K is used with the float32 epilogue only");
+  static_assert(EPI == EPI_F32 || EPI == EPI_UPDATE, "split-K only with the float32 or update epilogue");
   const int64_t m = blockIdx.y;
   const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (n >= P.N) return;
   const int64_t total = P.M * P.N;
   const float* src = P.partial + m * P.N + n;
+  if (EPI == EPI_UPDATE) {
+    const int64_t off = m * P.ldc + n;
+    const bool vec = ((P.N | P.ldc) & 3) == 0 && ((uintptr_t)P.partial & 15) == 0 &&
+                     (((uintptr_t)P.upd.p | (uintptr_t)P.upd.m | (uintptr_t)P.upd.v | (uintptr_t)P.upd.q) & 15) == 0 &&
+                     ((uintptr_t)P.upd.p16 & 7) == 0;
+    if (vec) {
+      f32x4 v = *reinterpret_cast<const f32x4*>(src);
+      for (int s = 1; s < P.splits; ++s) v += *reinterpret_cast<const f32x4*>(src + s * total);
+      apply_update4(P.upd, off, v);
+    } else {
+      for (int e = 0; e < 4 && n + e < P.N; ++e) {
+        float v = src[e];
+        for (int s = 1; s < P.splits; ++s) v += src[s * total + e];
+        apply_update(P.upd, off + e, v);
+      }
+    }
+    return;
+  }
   float* dst = reinterpret_cast<float*>(P.C) + m * P.ldc + n;
   const float* aux = P.aux ? reinterpret_cast<const float*>(P.aux) + m * P.ldc + n : nullptr;
   const bool vec = ((P.N | P.ldc) & 3) == 0 &&
@@ -367,7 +388,7 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   if (n_log >= (1ll << 31) - 8) return hipErrorInvalidValue;
   dim3 grid((unsigned)((n_log + 7) / 8 * 8));
   constexpr int NT = 64 * WGM * WGN;
-  if constexpr (EPI == EPI_F32) {
+  if constexpr (EPI == EPI_F32 || EPI == EPI_UPDATE) {
     if (P.splits > 1) {
       gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true, BKV><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
@@ -398,6 +419,9 @@ hipError_t dispatch_epi(const Gemm& g, const KArgs& P, hipStream_t s) {
     case EPI_F32: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_F32>(g, P, s);
     case EPI_BF16: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_BF16>(g, P, s);
     case EPI_GELU: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_GELU>(g, P, s);
+    case EPI_UPDATE:  // dW = dY^T X only: both operands m-major
+      if (g.a_kmajor || g.b_kmajor) return hipErrorInvalidValue;
+      return launch_tiles<BM, BN, WGM, WGN, STG, OCC, false, false, EPI_UPDATE, BKV>(P, g.batch, s);
     default: return dispatch_layout<BM, BN, WGM, WGN, STG, OCC, BKV, EPI_DGELU>(g, P, s);
   }
 }
@@ -427,6 +451,7 @@ KArgs make_args(const Gemm& g) {
   P.splits = 1;
   P.causal = g.causal;
   P.nz = g.batch;
+  P.upd = g.upd;
   return P;
 }
 
@@ -436,7 +461,11 @@ std::string gemm_check(const Gemm& g, bool f32_operands) {
   if (g.M < 0 || g.N < 0 || g.K < 0) return "negative GEMM dimension";
   if (!f32_operands && !g.a_kmajor && g.b_kmajor) return "m-major A with k-major B is not supported";
   if (g.batch < 1 || g.inner < 1) return "batch and inner must be >= 1";
-  if (!g.A || !g.B || !g.C) return "null GEMM operand";
+  if (!g.A || !g.B || (!g.C && g.epi != EPI_UPDATE)) return "null GEMM operand";
+  if (g.epi == EPI_UPDATE) {
+    if (!g.upd.p || !g.upd.m || !g.upd.q || (g.upd.adamw && !g.upd.v)) return "update epilogue needs p, m, (v) and q";
+    if (g.a_kmajor || g.b_kmajor || g.batch != 1) return "update epilogue only for dW = dY^T X";
+  }
   if (g.epi == EPI_GELU && !g.C2) return "GELU epilogue needs a second output";
   if (g.epi == EPI_DGELU && !g.aux) return "GELU-backward epilogue needs the pre-activation";
   const int64_t a_contig0 = g.a_kmajor ? g.K : g.M;
@@ -475,7 +504,7 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
   const int BM = kShapes[cfg].bm, BN = kShapes[cfg].bn;
   P.tiles_m = (int)cdiv(g.M, BM);
   P.tiles_n = (int)cdiv(g.N, BN);
-  if (splits > 1 && g.batch == 1 && g.splitk_ws && g.epi == EPI_F32 && g.M <= 65535) {
+  if (splits > 1 && g.batch == 1 && g.splitk_ws && (g.epi == EPI_F32 || g.epi == EPI_UPDATE) && g.M <= 65535) {
     while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
     if (splits > 1) {
       P.k_per_split = cdiv(cdiv(g.K, splits), 32) * 32;
@@ -507,7 +536,8 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
   auto tiles = [&](int bm, int bn) { return cdiv(g.M, bm) * cdiv(g.N, bn) * g.batch; };
-  const bool splittable = g.batch == 1 && g.K >= 1536 && g.epi == EPI_F32;
+  const bool f32_out = g.epi == EPI_F32 || g.epi == EPI_UPDATE;
+  const bool splittable = g.batch == 1 && g.K >= 1536 && f32_out;
   auto split_for = [&](int64_t t, int64_t want) {
     if (!splittable || t >= want) return 1;
     return (int)std::min<int64_t>(std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), g.K / 512), 8);
@@ -516,7 +546,7 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256)
     return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
   const int64_t t = tiles(128, 128);
-  if (g.epi == EPI_F32 && !g.b_kmajor && (g.a_kmajor || t < 128))
+  if (f32_out && !g.b_kmajor && (g.a_kmajor || t < 128))
     return launch_gemm_bf16_cfg(g, 3, split_for(t, 300), s);
   if (!g.a_kmajor) return launch_gemm_bf16_cfg(g, 1, splittable && t < 512 ? 4 : 1, s);
   return launch_gemm_bf16_cfg(g, 1, split_for(t, 512), s);

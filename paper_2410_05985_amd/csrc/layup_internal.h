@@ -49,7 +49,77 @@ enum Epilogue : int {
   EPI_BF16 = 1,   // C(bf16) = acc + bias
   EPI_GELU = 2,   // C(bf16) = acc + bias; C2(bf16) = gelu_tanh(acc + bias)
   EPI_DGELU = 3,  // C(bf16) = acc * gelu_tanh'(aux bf16)
+  EPI_UPDATE = 4, // acc is dW: local update + peer average of the weight (no C)
 };
+
+// Local optimizer update + peer average of one weight matrix, applied by the
+// dW GEMM (or its split-K sum) to the element it has just finished: the
+// weight gradient never goes to HBM.  Weight, optimizer state and peer copy
+// share the dW layout (row m, column n at m*ldc + n).
+struct UpdArgs {
+  float* p;
+  float* m;
+  float* v;        // AdamW only
+  const float* q;  // peer copy (pull form)
+  bf16_t* p16;     // bfloat16 copy of the weight
+  int32_t adamw;
+  float lr, mu, wd, b1, b2, eps, step_size, inv_sqrt_bc2, a, b, dfac, wdc;
+};
+// Scalars of the update for hyperparameters hp, mixing weight alpha and the
+// tensor's decay flag (bias corrections in double precision on the host).
+UpdArgs make_upd_args(const layup_hparams& hp, float alpha, bool decay);
+
+// The element update shared by the fused dW epilogues (same arithmetic as the
+// update+mix kernel: LibTorch SGD momentum or AdamW, then p <- a p1 + b q).
+__device__ __forceinline__ void apply_update(const UpdArgs& U, int64_t off, float g) {
+  float p = U.p[off], m = U.m[off], p1;
+  if (U.adamw) {
+    float v = U.v[off];
+    const float pd = p * U.dfac;
+    m = fmaf(U.b1, m, (1.0f - U.b1) * g);
+    v = fmaf(U.b2, v, (1.0f - U.b2) * (g * g));
+    const float den = fmaf(__builtin_amdgcn_sqrtf(v), U.inv_sqrt_bc2, U.eps);
+    p1 = fmaf(-U.step_size, m * __builtin_amdgcn_rcpf(den), pd);
+    U.v[off] = v;
+  } else {
+    const float gg = fmaf(U.wdc, p, g);
+    m = fmaf(U.mu, m, gg);
+    p1 = fmaf(-U.lr, m, p);
+  }
+  const float p2 = fmaf(U.a, p1, U.b * U.q[off]);
+  U.p[off] = p2;
+  U.m[off] = m;
+  if (U.p16) U.p16[off] = f2bf(p2);
+}
+
+// Four consecutive elements with 128-bit accesses (off a multiple of 4 and
+// every pointer 16-byte aligned; the bf16 copy 8-byte aligned).
+__device__ __forceinline__ void apply_update4(const UpdArgs& U, int64_t off, f32x4 g) {
+  f32x4 p = *reinterpret_cast<const f32x4*>(U.p + off), m = *reinterpret_cast<const f32x4*>(U.m + off);
+  const f32x4 q = *reinterpret_cast<const f32x4*>(U.q + off);
+  f32x4 p2;
+  if (U.adamw) {
+    f32x4 v = *reinterpret_cast<const f32x4*>(U.v + off);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float pd = p[e] * U.dfac;
+      m[e] = fmaf(U.b1, m[e], (1.0f - U.b1) * g[e]);
+      v[e] = fmaf(U.b2, v[e], (1.0f - U.b2) * (g[e] * g[e]));
+      const float den = fmaf(__builtin_amdgcn_sqrtf(v[e]), U.inv_sqrt_bc2, U.eps);
+      p2[e] = fmaf(U.a, fmaf(-U.step_size, m[e] * __builtin_amdgcn_rcpf(den), pd), U.b * q[e]);
+    }
+    *reinterpret_cast<f32x4*>(U.v + off) = v;
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      m[e] = fmaf(U.mu, m[e], fmaf(U.wdc, p[e], g[e]));
+      p2[e] = fmaf(U.a, fmaf(-U.lr, m[e], p[e]), U.b * q[e]);
+    }
+  }
+  *reinterpret_cast<f32x4*>(U.p + off) = p2;
+  *reinterpret_cast<f32x4*>(U.m + off) = m;
+  if (U.p16) *reinterpret_cast<u32x2*>(U.p16 + off) = u32x2{pack_bf2(p2[0], p2[1]), pack_bf2(p2[2], p2[3])};
+}
 
 struct Gemm {
   bool a_kmajor = true, b_kmajor = true;
@@ -74,6 +144,7 @@ struct Gemm {
   //   CAUSAL_A_LOWER: A(m, k) = 0 for k > m (P V, dS K): K stops at the tile's last row.
   //   CAUSAL_A_UPPER: A(m, k) = 0 for k < m (P^T dO, dS^T Q): K starts at the tile's first row.
   int causal = 0;
+  UpdArgs upd{};  // EPI_UPDATE
 };
 enum Causal : int { CAUSAL_NONE = 0, CAUSAL_OUT_LOWER = 1, CAUSAL_A_LOWER = 2, CAUSAL_A_UPPER = 3 };
 

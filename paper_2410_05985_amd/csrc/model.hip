@@ -153,6 +153,11 @@ struct layup_ctx {
   hipEvent_t ev_fwd_end = nullptr;     // end of the forward pass (loss gradient formed)
   hipEvent_t ev_join = nullptr;
   bool timeline_valid = false;
+  // fused dW update (schedule LAYUP_SCHEDULE_FUSED_DW) of the step in flight
+  bool fused_dw = false;
+  layup_hparams fused_hp{};
+  float fused_alpha = 0.f;
+  const float* fused_peer = nullptr;
   // optional timing of the linear layers' backward GEMMs (events around each)
   bool gemm_timing = false;
   std::vector<hipEvent_t> gt_events;  // start/stop pairs
@@ -290,6 +295,23 @@ struct Flat {
   float* g(const std::string& n) const { return c->buf.grads + find(c, n)->off; }
   bf16_t* w16(const std::string& n) const { return c->buf.params_bf16 + find(c, n)->off; }
 };
+
+// dW GEMM of weight matrix `name`: writes the gradient (EPI_F32), or, in the
+// fused schedule, applies the local update and peer average to the weight in
+// its epilogue (EPI_UPDATE; the gradient is not stored).
+Gemm dw_gemm(layup_ctx* c, Gemm g, const std::string& name) {
+  if (!c->fused_dw) return g;
+  const int64_t off = find(c, name)->off;
+  g.epi = EPI_UPDATE;
+  g.C = nullptr;
+  g.upd = make_upd_args(c->fused_hp, c->fused_alpha, true);
+  g.upd.p = c->buf.params + off;
+  g.upd.m = c->buf.m + off;
+  g.upd.v = c->buf.v ? c->buf.v + off : nullptr;
+  g.upd.q = c->fused_peer + off;
+  g.upd.p16 = c->buf.params_bf16 ? c->buf.params_bf16 + off : nullptr;
+  return g;
+}
 
 Gemm mk(bool ak, bool bk, int64_t M, int64_t N, int64_t K, const void* A, int64_t lda, const void* B,
         int64_t ldb, void* C, int64_t ldc, int epi) {
@@ -444,30 +466,37 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   const std::string p = "h" + std::to_string(l) + ".";
   float* dxo = c->dx[c->cur_dx];
   float* dxi = c->dx[c->cur_dx ^ 1];
+  // Every linear layer: dW, db and dX.  In the fused schedule dX runs first
+  // (it reads the weight before its update) and the dW GEMM updates the
+  // weight in place.
+  const bool fz = c->fused_dw;
   // MLP output projection
   // c->dy16 holds bf16(dxo), written by the LayerNorm backward that produced dxo
-  TRY(run_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32), s,
-               "mproj dW", true));
-  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "mproj.b"), s), "mproj db");
   Gemm dg = mk(true, false, N, F, d, c->dy16, d, fl.w16(p + "mproj.w"), F, c->df16, F, EPI_DGELU);
   dg.aux = A.f;
-  TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
+  if (fz) TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
+  TRY(run_gemm(c, dw_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
+                          p + "mproj.w"), s, "mproj dW", true));
+  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "mproj.b"), s), "mproj db");
+  if (!fz) TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
   // MLP input projection
-  TRY(run_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32), s,
-               "fc dW", true));
+  Gemm fcx = mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
+  if (fz) TRY(run_gemm(c, fcx, s, "fc dX", true));
+  TRY(run_gemm(c, dw_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
+                          p + "fc.w"), s, "fc dW", true));
   HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs(), fl.g(p + "fc.b"), s), "fc db");
-  TRY(run_gemm(c, mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32), s,
-               "fc dX", true));
+  if (!fz) TRY(run_gemm(c, fcx, s, "fc dX", true));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
                                  c->dy16, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
   // attention output projection
   // c->dy16 now holds bf16(dh) from the LayerNorm backward above
-  TRY(run_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32), s,
-               "proj dW", true));
+  Gemm prx = mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
+  if (fz) TRY(run_gemm(c, prx, s, "proj dX", true));
+  TRY(run_gemm(c, dw_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32),
+                          p + "proj.w"), s, "proj dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "proj.b"), s), "proj db");
-  TRY(run_gemm(c, mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16),
-               s, "proj dX", true));
+  if (!fz) TRY(run_gemm(c, prx, s, "proj dX", true));
   // attention core, batched over z = b*H + h
   auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
                      int64_t ci, int causal) {
@@ -505,11 +534,12 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
                              EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   // qkv projection
-  TRY(run_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
-                     EPI_F32), s, "qkv dW", true));
+  Gemm qx = mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
+  if (fz) TRY(run_gemm(c, qx, s, "qkv dX", true));
+  TRY(run_gemm(c, dw_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
+                                EPI_F32), p + "qkv.w"), s, "qkv dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs(), fl.g(p + "qkv.b"), s), "qkv db");
-  TRY(run_gemm(c, mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d,
-                     EPI_F32), s, "qkv dX", true));
+  if (!fz) TRY(run_gemm(c, qx, s, "qkv dX", true));
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
                                  l > 0 ? c->dy16 : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
                                  fl.g(p + "ln1.b"), N, (int)d,
@@ -569,8 +599,11 @@ layup_status mlp_backward(layup_ctx* c, int u) {
 // replica); peer16: its bfloat16 copy (push mode, nullable).
 void unit_tensors(layup_ctx* c, int u, float* peer, bf16_t* peer16, std::vector<UMTensor>& out) {
   out.clear();
+  // fused schedule: a block's weight matrices were updated by their dW GEMMs
+  const bool skip_mats = c->fused_dw && c->cfg.model == LAYUP_MODEL_GPT_BF16 && u >= 1 && u <= c->cfg.n_layer;
   for (int ti : c->L.unit_tensors[u]) {
     const TensorInfo& t = c->L.t[ti];
+    if (skip_mats && t.decay) continue;
     if (!out.empty()) {
       UMTensor& last = out.back();
       if (last.decay == t.decay && last.p + last.n == c->buf.params + t.off) {
@@ -900,8 +933,14 @@ layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* a) {
   if (!a) return fail(ctx, LAYUP_ERR_INVALID_ARG, "null step arguments");
   std::string m = check_hp(a->hp);
   if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
-  if (a->schedule != LAYUP_SCHEDULE_LAYERWISE && a->schedule != LAYUP_SCHEDULE_AFTER_BACKWARD)
+  if (a->schedule != LAYUP_SCHEDULE_LAYERWISE && a->schedule != LAYUP_SCHEDULE_AFTER_BACKWARD &&
+      a->schedule != LAYUP_SCHEDULE_FUSED_DW)
     return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown schedule");
+  const bool fused = a->schedule == LAYUP_SCHEDULE_FUSED_DW;
+  if (fused && ctx->cfg.model != LAYUP_MODEL_GPT_BF16)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the fused dW schedule is for the GPT model");
+  if (fused && (a->mix_mode != LAYUP_MIX_PULL || a->disagreement))
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the fused dW schedule mixes in pull form and reports no disagreement");
   float* peer = nullptr;
   bf16_t* peer16 = nullptr;
   const bool push = a->mix_mode == LAYUP_MIX_PUSH;
@@ -919,8 +958,16 @@ layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* a) {
   }
   TRY(layup_forward(ctx, a->tokens, a->x, a->loss_out));
   const int U = ctx->L.n_units;
+  ctx->fused_dw = fused;
+  ctx->fused_hp = *a->hp;
+  ctx->fused_alpha = a->alpha;
+  ctx->fused_peer = peer;
+  struct Reset {
+    layup_ctx* c;
+    ~Reset() { c->fused_dw = false; }
+  } reset{ctx};
   auto dis = [&](int u) { return a->disagreement ? a->disagreement + u : nullptr; };
-  if (a->schedule == LAYUP_SCHEDULE_LAYERWISE) {
+  if (a->schedule != LAYUP_SCHEDULE_AFTER_BACKWARD) {
     for (int u = U - 1; u >= 0; --u) {
       TRY(layup_layer_backward(ctx, u));
       TRY(unit_update(ctx, u, a->hp, a->alpha, peer, peer16, push, dis(u)));

@@ -177,6 +177,28 @@ __global__ void sum_partials_kernel(const float* part, int n, float* out) {
 
 int64_t update_mix_max_blocks() { return UM_MAX_BLOCKS; }
 
+UpdArgs make_upd_args(const layup_hparams& hp, float alpha, bool decay) {
+  UpdArgs U;
+  memset(&U, 0, sizeof(U));
+  U.adamw = hp.kind == LAYUP_ADAMW;
+  U.lr = hp.lr;
+  U.mu = hp.momentum;
+  U.wd = hp.weight_decay;
+  U.b1 = hp.beta1;
+  U.b2 = hp.beta2;
+  U.eps = hp.eps;
+  if (U.adamw) {
+    const double t = (double)hp.step;
+    U.step_size = (float)((double)hp.lr / (1.0 - pow((double)hp.beta1, t)));
+    U.inv_sqrt_bc2 = (float)(1.0 / sqrt(1.0 - pow((double)hp.beta2, t)));
+  }
+  U.a = (float)(1.0 - (double)alpha);
+  U.b = alpha;
+  U.dfac = decay ? (1.0f - hp.lr * hp.weight_decay) : 1.0f;
+  U.wdc = decay ? hp.weight_decay : 0.0f;
+  return U;
+}
+
 template <int OPT, bool DIS>
 static void launch_um(bool push, int64_t grid, const UMArgs& A, int64_t chunks, hipStream_t stream) {
   if (push) update_mix_kernel<OPT, DIS, true><<<grid, UM_THREADS, 0, stream>>>(A, chunks);

@@ -22,7 +22,7 @@ LAYUP_SGD_MOMENTUM, LAYUP_ADAMW = 0, 1
 LAYUP_MODEL_MLP_F32, LAYUP_MODEL_GPT_BF16 = 0, 1
 LAYUP_MAX_MLP_LAYERS = 8
 LAYUP_MIX_PULL, LAYUP_MIX_PUSH = 0, 1
-LAYUP_SCHEDULE_LAYERWISE, LAYUP_SCHEDULE_AFTER_BACKWARD = 0, 1
+LAYUP_SCHEDULE_LAYERWISE, LAYUP_SCHEDULE_AFTER_BACKWARD, LAYUP_SCHEDULE_FUSED_DW = 0, 1, 2
 
 STATUS_NAMES = {0: "OK", 1: "INVALID_ARG", 2: "SHAPE", 3: "ALIGN", 4: "DTYPE", 5: "STATE", 6: "HIP"}
 

@@ -100,6 +100,9 @@ GPT_TEST_RAGGED = GPTConfig(n_layer=2, d_model=96, n_head=3, d_ff=384, seq=80,
 # 48, which the fused attention kernels do not cover (score GEMM + softmax).
 GPT_TEST_DH128 = GPTConfig(n_layer=1, d_model=256, n_head=2, d_ff=512, seq=96, batch=2,
                            vocab=300, name="gpt-test-dh128")
+# 2048 tokens: enough K for the split-K dW GEMMs (their float32 partial sums).
+GPT_TEST_LONG = GPTConfig(n_layer=1, d_model=128, n_head=2, d_ff=256, seq=512, batch=4,
+                          vocab=400, name="gpt-test-long")
 GPT_TEST_DH48 = GPTConfig(n_layer=1, d_model=96, n_head=2, d_ff=256, seq=64, batch=2,
                           vocab=200, name="gpt-test-dh48")
 

@@ -310,3 +310,59 @@ def test_gemm_timing_counts_the_block_backward_gemms():
     LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0)
     assert LU.layup_gemm_timing_read(m.ctx)[1] == 0
     m.close()
+
+
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_LONG], ids=lambda c: c.name)
+def test_fused_dw_schedule_matches_oracle(cfg):
+    """The fused schedule (each block's weight matrices updated and mixed by
+    their dW GEMM, in its epilogue or, with 2048 tokens, in its split-K sum):
+    parameters and AdamW moments against the oracle's layer-wise step as in
+    test_gpt_step_parity, the order trace unchanged, and the bf16 copy equal
+    to the nearest-even bf16 of the updated float32 weights."""
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, ohp = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    torch.cuda.synchronize()
+    LU.layup_step_ex(m.ctx, td, None, hp, cfg.alpha, schedule=LU.LAYUP_SCHEDULE_FUSED_DW, loss_out=loss)
+    op = {k: v.astype(np.float64) for k, v in params.items()}
+    om = {k: np.zeros_like(v) for k, v in op.items()}
+    ov = {k: np.zeros_like(v) for k, v in op.items()}
+    opeer = {k: v.astype(np.float64) for k, v in peers[0].items()}
+    oloss, ograds, otrace, _ = O.gpt_step(op, om, ov, opeer, tokens, cfg.n_head, ohp, cfg.alpha)
+    m.synchronize()
+    assert abs(loss.item() - oloss) <= 2e-3 * abs(oloss)
+    got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
+    for k in op:
+        shp = got_p[k].shape
+        check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
+                           f"param {k}")
+        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}")
+        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}")
+    assert m.read_trace() == [(0, u) for u in otrace]
+    p16 = (m.params_bf16.to(torch.int32) << 16).view(torch.float32).cpu().numpy()
+    assert np.array_equal(p16, O.bf16(m.params.cpu().numpy().astype(np.float64)))
+    m.close()
+
+
+def test_fused_dw_schedule_argument_checks():
+    cfg = S.GPT_TEST
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, _ = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    dis = torch.zeros(m.n_units, dtype=torch.float32, device=DEV)
+    with pytest.raises(LU.LayupError):
+        LU.layup_step_ex(m.ctx, td, None, hp, 0.5, schedule=LU.LAYUP_SCHEDULE_FUSED_DW, disagreement=dis)
+    other = torch.zeros_like(m.params)
+    with pytest.raises(LU.LayupError):
+        LU.layup_step_ex(m.ctx, td, None, hp, 0.5, schedule=LU.LAYUP_SCHEDULE_FUSED_DW,
+                         mix_mode=LU.LAYUP_MIX_PUSH, push_params=other)
+    m.close()
+    mcfg = S.MLP_TINY
+    mm = LU.Model(LU.mlp_config(mcfg.dims, mcfg.batch), "sgd")
+    x, y = S.mlp_inputs(mcfg)
+    with pytest.raises(LU.LayupError):
+        LU.layup_step_ex(mm.ctx, torch.from_numpy(y[0]).to(DEV), torch.from_numpy(x[0]).to(DEV),
+                         LU.hparams("sgd", mcfg.lr, mcfg.momentum, 0.0), 0.5,
+                         schedule=LU.LAYUP_SCHEDULE_FUSED_DW)
+    mm.close()
