@@ -74,10 +74,13 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
 //    r*64 + 16*(c ^ ((r >> 2) & 3)).  Sixteen lanes reading one chunk of 16
 //    consecutive rows (the MFMA operand read, ds_read_b128) cover all banks.
 //  m-major operand, 32 x ROWS (k rows of ROWS elements): chunk c of k-row kk at
-//    kk*2*ROWS + 16*(c ^ sw(kk)), sw(kk) = ((kk & 3) << 2) & (ROWS/8 - 1).  The
-//    operand is read with ds_read_b64_tr_b16: within each 16-lane group, lane
-//    s supplies 4 consecutive m of k-row kb + s/4 and receives, transposed,
-//    4 consecutive k of one m.
+//    kk*2*ROWS + 16*(c ^ sw(kk)).  The operand is read with ds_read_b64_tr_b16:
+//    within each 16-lane group, lane s supplies 4 consecutive m of k-row
+//    kb + s/4 and receives, transposed, 4 consecutive k of one m, so four
+//    consecutive k-rows are read at one chunk position.  sw spreads those rows
+//    over the 256-byte bank cycle: ((kk & 3) << 2) & (ROWS/8 - 1) for
+//    power-of-two ROWS; none for ROWS = 96 (a 192-byte row stride already
+//    staggers them); 4 on the odd pairs for ROWS = 192 (384-byte stride).
 __device__ __forceinline__ constexpr int kswz(int r, int bkv) {
   // 16 consecutive rows of 2*bkv bytes must cover the 256-byte bank cycle once
   return (r / (128 / bkv)) % (bkv / 8);
@@ -85,7 +88,13 @@ __device__ __forceinline__ constexpr int kswz(int r, int bkv) {
 template <int BKV>
 __device__ __forceinline__ int km_off(int r, int c) { return r * 2 * BKV + 16 * (c ^ kswz(r, BKV)); }
 template <int ROWS>
-__device__ __forceinline__ int mm_sw(int kk) { return ((kk & 3) << 2) & (ROWS / 8 - 1); }
+__device__ __forceinline__ int mm_sw(int kk) {
+  static_assert(ROWS % 32 == 0 && (ROWS & (ROWS - 1)) == 0 || ROWS == 96 || ROWS == 192,
+                "m-major tile width without a bank swizzle");
+  if (ROWS == 96) return 0;
+  if (ROWS == 192) return (kk & 2) << 1;
+  return ((kk & 3) << 2) & (ROWS / 8 - 1);
+}
 template <int ROWS>
 __device__ __forceinline__ int mm_off(int kk, int c) { return kk * 2 * ROWS + 16 * (c ^ mm_sw<ROWS>(kk)); }
 
@@ -113,8 +122,9 @@ __device__ __forceinline__ void issue_tile(const bf16_t* base, int64_t ld, int64
       src = base + gr * ld + gk;
     } else {
       constexpr int LPR = ROWS / 8;           // 16-byte chunks per k-row
-      const int kk = blk * (64 / LPR) + lane / LPR;
-      const int c = (lane % LPR) ^ mm_sw<ROWS>(kk);
+      const int q = blk * 64 + lane;           // chunk slot in the tile
+      const int kk = q / LPR;
+      const int c = (q % LPR) ^ mm_sw<ROWS>(kk);
       const int64_t gk = min(k0 + kk, K - 1);
       const int64_t gm = min(r0 + 8 * c, R - 8);
       src = base + gk * ld + gm;
@@ -140,25 +150,82 @@ __device__ __forceinline__ void zero_tail(char* lds, int krem) {
   }
 }
 
-// One 32x32x16 MFMA operand fragment: rows rb..rb+31 (lane % 32), k values
-// ks*16 + 8*(lane/32) .. +7 of the tile.
+// ---- operand fragments.  One 32x32x16 MFMA operand fragment holds rows
+// rb..rb+31 (lane % 32) and k values ks*16 + 8*(lane/32) .. +7 of the tile.
+// The LDS reads are issued as inline assembly with explicit lgkmcnt waits:
+// the compiler cannot tell an LDS read apart from the direct-to-LDS copies in
+// flight into other stages, and before a transposing read it would wait for
+// every outstanding copy (vmcnt(0)), which serializes the copy pipeline.
+// Offsets are compile-time immediates where they are lane-independent.
+template <int N>
+struct IntC { static constexpr int value = N; };
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(IntC<I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x4 lds_read_b128(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "LDS immediate offset");
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
+  return v;
+}
+
+template <int OFF>
+__device__ __forceinline__ u32x2 lds_read_tr(uint32_t a) {
+  static_assert(OFF >= 0 && OFF < 65536, "LDS immediate offset");
+  u32x2 v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
+  return v;
+}
+
+// Wait until at most N LDS reads are outstanding (LDS reads return in order).
+template <int N>
+__device__ __forceinline__ void lgkm_wait() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N < 15 ? N : 15));
+}
+
+// Make the MFMA that consumes v depend on the preceding wait.
+__device__ __forceinline__ void after_wait(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+// Per-lane part of the LDS offset of a fragment.  k-major: one value per
+// K sub-step (the 32-row blocks are whole-row multiples apart, which the
+// swizzle leaves alone); m-major: one value per 32-column block (the sub-step
+// and the second half of the k range are whole k-rows apart).
 template <int ROWS, bool KMAJOR, int BKV>
-__device__ __forceinline__ bf16x8 frag(const char* lds, int rb, int ks, int lane) {
+__device__ __forceinline__ uint32_t frag_lane_off(int rb, int idx, int lane) {
   if (KMAJOR) {
-    const int r = rb + (lane & 31);
-    return *reinterpret_cast<const bf16x8*>(lds + km_off<BKV>(r, 2 * ks + (lane >> 5)));
+    return km_off<BKV>(rb + (lane & 31), 2 * idx + (lane >> 5));
   } else {
     const int g = lane >> 4, s = lane & 15;
-    const int kb = ks * 16 + 8 * (g >> 1) + (s >> 2);
-    const int m = rb + 16 * (g & 1) + 4 * (s & 3);
-    const int c = m >> 3, half = (m & 7) * 2;
-    v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) v4i16*)LDS_PTR(lds + mm_off<ROWS>(kb, c) + half));
-    v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-        (__attribute__((address_space(3))) v4i16*)LDS_PTR(lds + mm_off<ROWS>(kb + 4, c) + half));
-    v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-    return __builtin_bit_cast(bf16x8, v);
+    const int kb = 8 * (g >> 1) + (s >> 2);
+    const int m = rb + 32 * idx + 16 * (g & 1) + 4 * (s & 3);
+    return mm_off<ROWS>(kb, m >> 3) + (m & 7) * 2;
   }
+}
+
+// Issue the LDS reads of the T fragments of sub-step KSI of one operand.
+// sb: stage base + operand base; off: frag_lane_off values.
+template <int ROWS, bool KMAJOR, int BKV, int T, int KSI>
+__device__ __forceinline__ void read_frags(uint32_t sb, const uint32_t* off, u32x4* f) {
+  static_for<0, T>([&](auto I) {
+    constexpr int i = decltype(I)::value;
+    if constexpr (KMAJOR) {
+      f[i] = lds_read_b128<i * 32 * 2 * BKV>(sb + off[KSI]);
+    } else {
+      const u32x2 lo = lds_read_tr<KSI * 16 * 2 * ROWS>(sb + off[i]);
+      const u32x2 hi = lds_read_tr<KSI * 16 * 2 * ROWS + 4 * 2 * ROWS>(sb + off[i]);
+      f[i] = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+  });
 }
 
 // s_waitcnt vmcnt(n), expcnt and lgkmcnt left alone (gfx9 encoding).
@@ -237,6 +304,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // per-lane fragment offsets inside a stage (B after A)
+  constexpr int NA = AK ? KS : TM, NB = BKM ? KS : TN;
+  uint32_t a_off[NA], b_off[NB];
+#pragma unroll
+  for (int x = 0; x < NA; ++x) a_off[x] = frag_lane_off<BM, AK, BKV>(wm * WM, x, lane);
+#pragma unroll
+  for (int x = 0; x < NB; ++x) b_off[x] = A_BYTES + frag_lane_off<BN, BKM, BKV>(wn * WN, x, lane);
+  // LDS reads issued per sub-step
+  constexpr int NREAD = TM * (AK ? 1 : 2) + TN * (BKM ? 1 : 2);
+  const uint32_t lds0 = lds_addr(smem);
+
   const int nk = (int)((ke - kb + BKV - 1) / BKV);
   const int krem = (int)((ke - kb) - (int64_t)(nk - 1) * BKV);  // valid k in the last step
   auto issue = [&](int t) {
@@ -252,7 +330,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   for (int kt = 0; kt < nk; ++kt) {
     // tile kt has landed once at most the loads of the younger tiles are
     // outstanding; the barrier publishes every wave's copies and frees the
-    // stage that was read in the previous step
+    // stage that was read in the previous step (every wave has waited for
+    // its reads of that stage before its last MFMAs)
     const int younger = min(STAGES - 2, nk - 1 - kt);
     if (younger >= 2) WAIT_VMCNT(2 * LOADS);
     else if (younger == 1) WAIT_VMCNT(LOADS);
@@ -265,28 +344,32 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
       __syncthreads();
     }
     if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const uint32_t sb = lds0 + (uint32_t)((kt % STAGES) * STAGE);
     // operand fragments of sub-step ks+1 are read while the MFMAs of ks run
-    bf16x8 af[2][TM], bfr[2][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i) af[0][i] = frag<BM, AK, BKV>(st, wm * WM + i * 32, 0, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bfr[0][j] = frag<BN, BKM, BKV>(st + A_BYTES, wn * WN + j * 32, 0, lane);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int cb = ks & 1;
-      if (ks + 1 < KS) {
-#pragma unroll
-        for (int i = 0; i < TM; ++i) af[cb ^ 1][i] = frag<BM, AK, BKV>(st, wm * WM + i * 32, ks + 1, lane);
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfr[cb ^ 1][j] = frag<BN, BKM, BKV>(st + A_BYTES, wn * WN + j * 32, ks + 1, lane);
+    u32x4 af[2][TM], bfr[2][TN];
+    read_frags<BM, AK, BKV, TM, 0>(sb, a_off, af[0]);
+    read_frags<BN, BKM, BKV, TN, 0>(sb, b_off, bfr[0]);
+    static_for<0, KS>([&](auto KSI) {
+      constexpr int ks = decltype(KSI)::value, cb = ks & 1;
+      if constexpr (ks + 1 < KS) {
+        read_frags<BM, AK, BKV, TM, ks + 1>(sb, a_off, af[cb ^ 1]);
+        read_frags<BN, BKM, BKV, TN, ks + 1>(sb, b_off, bfr[cb ^ 1]);
+        lgkm_wait<NREAD>();
+      } else {
+        lgkm_wait<0>();
       }
+#pragma unroll
+      for (int i = 0; i < TM; ++i) after_wait(af[cb][i]);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) after_wait(bfr[cb][j]);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cb][i], bfr[cb][j], acc[i][j], 0, 0, 0);
-    }
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[cb][i]),
+                                                              __builtin_bit_cast(bf16x8, bfr[cb][j]),
+                                                              acc[i][j], 0, 0, 0);
+    });
   }
 
   // ---- epilogue.  32x32 accumulator layout: lane l, register r holds
