@@ -327,11 +327,15 @@ layup_status layup_push_sum_receive(double* w, int32_t n_workers, int32_t sender
 
 /* Saved forward activation of the context, for inspection (device pointer
  * into the workspace).  which: 0 = block input x (f32), 1 = LN1 out (bf16),
- * 2 = qkv (bf16), 3 = attention probabilities (bf16), 4 = attention output
+ * 2 = qkv (bf16), 3 = attention probabilities (bf16, [B][H][T][T]; stored
+ * only when the head width is not 32, 64 or 128), 4 = attention output
  * (bf16), 5 = residual after attention (f32), 6 = LN2 out (bf16), 7 = MLP
  * pre-activation (bf16), 8 = GELU out (bf16), 9 = final LN out (bf16),
- * 10 = logit gradient (bf16), 11 = final residual (f32).  layer is the
- * block index for 0..8.  dtype_out: 0 = f32, 1 = bf16. */
+ * 10 = logit gradient (bf16), 11 = final residual (f32), 12 = base-2
+ * log-sum-exp of each query's scaled causal scores (f32, [B][H][T]; fused
+ * attention, head width 32, 64 or 128, only).  layer is the block index for
+ * 0..8 and 12.  dtype_out: 0 = f32, 1 = bf16.  Asking for an activation the
+ * configuration does not store is LAYUP_ERR_INVALID_ARG. */
 layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, const void** ptr,
                               int64_t* numel, int32_t* dtype_out);
 

@@ -132,6 +132,16 @@ def causal_softmax(s: Array) -> Array:
     return e / e.sum(axis=-1, keepdims=True)
 
 
+def causal_logsumexp(s: Array) -> Array:
+    """Natural log of the causal softmax normaliser of every row of s [.., T, T]:
+    log sum_{j <= i} exp(s_ij).  exp(s_ij - lse_i) is causal_softmax(s)_ij."""
+    t = s.shape[-1]
+    mask = np.triu(np.ones((t, t), dtype=bool), k=1)
+    z = np.where(mask, -np.inf, s)
+    mx = z.max(axis=-1, keepdims=True)
+    return (mx + np.log(np.exp(z - mx).sum(axis=-1, keepdims=True)))[..., 0]
+
+
 def softmax_bwd(p: Array, dp: Array) -> Array:
     """Backward of a row softmax: ds = p * (dp - rowsum(dp * p))."""
     return p * (dp - (dp * p).sum(axis=-1, keepdims=True))
@@ -377,6 +387,7 @@ def gpt_forward(params, tokens, n_head: int, rnd: Callable = bf16):
         v = _heads(qkv[:, 2 * d:], bsz, t, n_head, dh)
         s = (q @ k.swapaxes(-1, -2)) * scale
         c["P"] = P = rnd(causal_softmax(s))
+        c["lse"] = causal_logsumexp(s)
         c["o"] = o = rnd(_unheads(P @ v))
         h_res = x + linear_fwd(o, rnd(params[p + "proj.w"]), params[p + "proj.b"])
         c["h"] = h_res

@@ -1,35 +1,36 @@
-// Fused causal attention core of a GPT block on the CDNA4 matrix cores: the
-// forward P = softmax(Q K^T / sqrt(dh)), O = P V and the backward part that
-// needs the score matrix, dS = P (dP - rowsum(dP P)) / sqrt(dh) with
-// dP = dO V^T, and dQ = dS K.  The score and dP matrices live only in
-// registers; P (the saved activation) and dS (read by the dK = dS^T Q GEMM)
-// are written once in bfloat16, at the same rounding points as the unfused
-// kernels (P and dS rounded after normalisation/scaling, O and dQ rounded
-// from float32 accumulations).
+// Fused causal attention core of a GPT block on the CDNA4 matrix cores,
+// flash-attention style: the score matrix S = Q K^T / sqrt(dh), its softmax P
+// and, in the backward, dP = dO V^T and dS = P (dP - rowsum(dP P)) / sqrt(dh)
+// live only in registers; no T x T matrix is stored.
 //
-// A workgroup of four waves owns 128 consecutive queries of one (batch,
-// head), one wave per 32 queries, and walks the key tiles of 32 keys up to
-// its last diagonal.  Each K and V tile is loaded once per workgroup
-// (coalesced, through registers) into double-buffered LDS and read by all
-// four waves; a wave computes only the tiles up to its own diagonal.
+//  - Forward: one pass over the keys with the running (online) row maximum
+//    and sum; O accumulates unnormalised and is divided by the row sum at the
+//    end.  Stored: O (bf16, the next GEMM's operand), O in float32 and the
+//    base-2 log-sum-exp of each query's scaled scores.
+//  - Backward, two kernels, every output written by one workgroup in a fixed
+//    order (deterministic): (1) per block of queries, P and dS are recomputed
+//    from Q, K, V, dO and the log-sum-exp and dQ = dS K accumulates; this
+//    kernel also stores D = rowsum(dP P) = dO . O (from the float32 O).
+//    (2) per block of keys, P and dS are recomputed again and dV = P^T dO and
+//    dK = dS^T Q accumulate.
 //
-// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16:
-// in the accumulator every lane then holds one query (lane % 32) and 16 of
-// the tile's keys, so the row statistics of a query are a reduction over the
-// lane's registers plus one exchange with lane l ^ 32.  The same registers,
-// rounded to bfloat16, are the B operand of the next product O^T = V^T P^T
-// (and dQ^T = K^T dS^T): lane half h holds keys 4h..4h+3 and 8+4h..8+4h+3 of
-// each 16-key step, and the A operand (V^T or K^T) is read from its LDS tile
-// with the transposing LDS read in exactly that key order.  The outputs O^T
-// and dQ^T again give each lane one query, stored with 8-byte row segments.
+// A workgroup of four waves owns 128 consecutive queries (forward, dQ) or
+// keys (dK/dV) of one (batch, head), 32 per wave, and walks the other
+// operand in steps of 64 rows (two 32-row sub-tiles), staged through
+// registers into double-buffered LDS and shared by the four waves.  Products
+// use v_mfma_f32_32x32x16_bf16.  The score block is computed so that every
+// lane owns one of the wave's 32 rows (a query in the forward and dQ
+// kernels, S^T = K Q^T; a key in the dK/dV kernel, S = Q K^T) and 16 of the
+// sub-tile's other index; those registers, rounded to bfloat16, are directly
+// the B operand of the next product (O^T = V^T P^T, dQ^T = K^T dS^T,
+// dV^T = dO^T P, dK^T = Q^T dS): lane half h holds indices 4h..4h+3 and
+// 8+4h..8+4h+3 of each 16-step, and the A operand is read from its LDS tile
+// with the transposing LDS read in exactly that order.
 //
-// The forward makes two passes over the keys: row maximum and sum first,
-// then the normalised P, which is stored and multiplied with V.  The
-// backward takes rowsum(dP P) as dO . O from the float32 O the forward keeps
-// (equal in exact arithmetic, since O = P V).  Entries above the diagonal,
-// up to the end of the query's 128-row band, are written as zeros: the
-// batched dV = P^T dO and dK = dS^T Q GEMMs read whole 128-wide diagonal
-// tiles.
+// Exponentials are base 2 on scores pre-multiplied by scale * log2(e).  The
+// backward recomputes P in float32 and rounds it to bfloat16 before both of
+// its uses (dV = P^T dO and dS = P (dP - D)), the precision at which an
+// unfused implementation would have stored it.
 #include "layup_internal.h"
 
 namespace layup {
@@ -39,18 +40,20 @@ namespace {
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 #define AT_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
-constexpr int AT_WAVES = 4;              // waves per workgroup, 32 queries each
+constexpr int AT_WAVES = 4;              // waves per workgroup, 32 rows each
 constexpr int AT_THREADS = 64 * AT_WAVES;
-constexpr int AT_ZERO_BAND = 128;        // row band of the batched attention GEMMs' tiles
+constexpr int AT_STEP = 64;              // rows of the walked operand per step (two sub-tiles)
 
-// LDS tile of 32 keys x DH columns (key rows of 2*DH bytes) in one of two
+// LDS tile of AT_STEP rows x DH columns (rows of 2*DH bytes) in one of two
 // layouts, both swizzling 16-byte chunks within a row:
-//  - row-read tile (A operand of S^T = K Q^T and dP^T = V dO^T; lane reads
-//    16 bytes of key row lane % 32): chunk c of row r at c ^ ((r / (128/DH)) % (DH/8)),
-//    so 16 consecutive rows cover the 256-byte bank cycle once;
-//  - transposed-read tile (A operand of O^T = V^T P^T and dQ^T = K^T dS^T):
-//    chunk c of row r at c ^ (((r & 3) << 2) & (DH/8 - 1)), so the four rows
-//    of one transposing read fall on different banks.
+//  - row-read tile (A operand whose rows are the tile rows; lane reads 16
+//    bytes of row lane % 32 of a sub-tile): chunk c of row r at
+//    c ^ ((r / (128/DH)) % (DH/8)), so 16 consecutive rows cover the 256-byte
+//    bank cycle once;
+//  - transposed-read tile (A operand whose rows are the tile columns): chunk
+//    c of row r at c ^ (((r & 3) << 2) & (DH/8 - 1)), so the four rows of one
+//    transposing read fall on different banks.
+// Both swizzles repeat every 32 rows, so a sub-tile is a fixed offset.
 template <int DH>
 __device__ __forceinline__ int row_off(int r, int c) {
   return r * 2 * DH + 16 * (c ^ ((r / (128 / DH)) % (DH / 8)));
@@ -60,42 +63,55 @@ __device__ __forceinline__ int tr_off(int r, int c) {
   return r * 2 * DH + 16 * (c ^ (((r & 3) << 2) & (DH / 8 - 1)));
 }
 
-// One 32-key tile staged in registers by the whole workgroup: 16-byte chunk
-// idx = thread + AT_THREADS * i is chunk idx % (DH/8) of key row idx / (DH/8).
-template <int DH>
+// One tile of ROWS rows staged in registers by the whole workgroup: 16-byte
+// chunk idx = thread + AT_THREADS * i is chunk idx % (DH/8) of row idx / (DH/8).
+template <int DH, int ROWS>
 struct Stage {
   static constexpr int LPR = DH / 8;
-  static constexpr int CHUNKS = 32 * LPR;
+  static constexpr int CHUNKS = ROWS * LPR;
   static constexpr int PER = (CHUNKS + AT_THREADS - 1) / AT_THREADS;
   u32x4 v[PER];
 };
 
-template <int DH>
-__device__ __forceinline__ void fetch(Stage<DH>& st, const bf16_t* m, int64_t ld, int k0, int T) {
+// rows r0.. of a row-major matrix with leading dimension ld (rows past T
+// read row T - 1; they only feed masked products)
+template <int DH, int ROWS>
+__device__ __forceinline__ void fetch(Stage<DH, ROWS>& st, const bf16_t* m, int64_t ld, int r0, int T) {
 #pragma unroll
-  for (int i = 0; i < Stage<DH>::PER; ++i) {
+  for (int i = 0; i < Stage<DH, ROWS>::PER; ++i) {
     const int idx = threadIdx.x + AT_THREADS * i;
-    if (idx < Stage<DH>::CHUNKS) {
-      const int r = idx / Stage<DH>::LPR, c = idx % Stage<DH>::LPR;
-      st.v[i] = *reinterpret_cast<const u32x4*>(m + (int64_t)min(k0 + r, T - 1) * ld + 8 * c);
+    if (idx < Stage<DH, ROWS>::CHUNKS) {
+      const int r = idx / Stage<DH, ROWS>::LPR, c = idx % Stage<DH, ROWS>::LPR;
+      st.v[i] = *reinterpret_cast<const u32x4*>(m + (int64_t)min(r0 + r, T - 1) * ld + 8 * c);
     }
   }
 }
 
-template <int DH, bool TR>
-__device__ __forceinline__ void put(const Stage<DH>& st, char* lds) {
+template <int DH, int ROWS, bool TR>
+__device__ __forceinline__ void put(const Stage<DH, ROWS>& st, char* lds) {
 #pragma unroll
-  for (int i = 0; i < Stage<DH>::PER; ++i) {
+  for (int i = 0; i < Stage<DH, ROWS>::PER; ++i) {
     const int idx = threadIdx.x + AT_THREADS * i;
-    if (idx < Stage<DH>::CHUNKS) {
-      const int r = idx / Stage<DH>::LPR, c = idx % Stage<DH>::LPR;
+    if (idx < Stage<DH, ROWS>::CHUNKS) {
+      const int r = idx / Stage<DH, ROWS>::LPR, c = idx % Stage<DH, ROWS>::LPR;
       *reinterpret_cast<u32x4*>(lds + (TR ? tr_off<DH>(r, c) : row_off<DH>(r, c))) = st.v[i];
     }
   }
 }
 
+// Before the step loop: every load issued so far (the wave's own operand
+// rows and the first tile) complete, so the compiler's wait counting enters
+// the loop with nothing outstanding and waits inside it only for what the
+// loop issues.
+__device__ __forceinline__ void loop_entry_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(0);  // vmcnt(0) expcnt(0) lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // LDS stores of this wave done, then the workgroup barrier (no wait on the
-// vector-memory counter: outstanding P/dS stores are left in flight).
+// vector-memory counter: the next tile's loads stay in flight).
 __device__ __forceinline__ void tile_barrier() {
   __builtin_amdgcn_sched_barrier(0);
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
@@ -103,18 +119,19 @@ __device__ __forceinline__ void tile_barrier() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// A operand of S^T = K Q^T (or dP^T = V dO^T) from a row-read tile: key row
-// lane % 32, columns 16 ks + 8 (lane / 32) .. +7.
+// A operand from a row-read tile: row 32*sub + lane % 32 of the tile,
+// columns 16 ks + 8 (lane / 32) .. +7.
 template <int DH>
-__device__ __forceinline__ bf16x8 row_frag(const char* lds, int ks, int lane) {
-  return *reinterpret_cast<const bf16x8*>(lds + row_off<DH>(lane & 31, 2 * ks + (lane >> 5)));
+__device__ __forceinline__ bf16x8 row_frag(const char* lds, int sub, int ks, int lane) {
+  return *reinterpret_cast<const bf16x8*>(lds + row_off<DH>(32 * sub + (lane & 31), 2 * ks + (lane >> 5)));
 }
 
-// A operand (rows m = tile columns rb..rb+31; k = 16 keys of step ks) from a
-// transposed-read tile, in the key order of the S^T accumulator: lane half h
-// takes keys ks*16 + 4h + 0..3 and ks*16 + 8 + 4h + 0..3.  Transposing read:
-// lane s of a 16-lane group addresses key row kb + s/4, columns m..m+3, and
-// receives column rb + 16*(group & 1) + s of four consecutive key rows.
+// A operand (rows m = tile columns rb..rb+31; k = 16 tile rows of step ks,
+// ks = 0..3 over the 64-row tile) from a transposed-read tile, in the row
+// order of a score accumulator: lane half h takes rows ks*16 + 4h + 0..3 and
+// ks*16 + 8 + 4h + 0..3.  Transposing read: lane s of a 16-lane group
+// addresses tile row kb + s/4, columns m..m+3, and receives column
+// rb + 16*(group & 1) + s of four consecutive tile rows.
 template <int DH>
 __device__ __forceinline__ bf16x8 tr_frag(const char* lds, int rb, int ks, int lane) {
   const int g = lane >> 4, s = lane & 15;
@@ -137,50 +154,87 @@ __device__ __forceinline__ bf16x8 pack8(const float* v) {
   return __builtin_bit_cast(bf16x8, w);
 }
 
-// Key of accumulator register r for lane half h, relative to the tile start.
+// Key (or query) of accumulator register r for lane half h, relative to the
+// 32-row sub-tile start.
 __device__ __forceinline__ int acc_key(int r, int h) { return (r >> 2) * 8 + 4 * h + (r & 3); }
 
-// Work of a workgroup: 128 queries of one (batch, head), heaviest first.
-struct Item {
+// ---- workgroup items
+// Forward and dQ: 128 queries of one (batch, head), heaviest (last) first.
+struct QItem {
   int qb;    // this wave's 32-query block
-  int nkt;   // key tiles the workgroup walks
-  int mine;  // key tiles this wave computes (0 past the sequence end)
+  int nst;   // key steps the workgroup walks
+  int mine;  // key steps this wave computes (0 past the sequence end)
   int b, hh;
 };
-__device__ __forceinline__ bool item_of(int T, int B, int H, Item& it) {
+__device__ __forceinline__ bool q_item(int T, int B, int H, QItem& it) {
   const int nqb = (T + 31) / 32, nqg = (nqb + AT_WAVES - 1) / AT_WAVES;
   const int64_t id = blockIdx.x;
   if (id >= (int64_t)nqg * B * H) return false;
   const int z = (int)(id % (B * H));
   const int qg = nqg - 1 - (int)(id / (B * H));
   it.qb = qg * AT_WAVES + (int)(threadIdx.x >> 6);
-  it.nkt = min(nqb, (qg + 1) * AT_WAVES);
-  it.mine = it.qb < nqb ? it.qb + 1 : 0;
+  it.nst = (min(T, (qg + 1) * AT_WAVES * 32) - 1) / AT_STEP + 1;
+  it.mine = it.qb < nqb ? (min(T, it.qb * 32 + 32) - 1) / AT_STEP + 1 : 0;
+  it.b = z / H;
+  it.hh = z % H;
+  return true;
+}
+// dK/dV: 128 keys of one (batch, head), heaviest (first) first.
+struct KItem {
+  int kb;     // this wave's 32-key block
+  int first;  // first query step of the workgroup
+  int mine;   // first query step this wave computes
+  int nst;    // query steps (to the end of the sequence)
+  bool active;
+  int b, hh;
+};
+__device__ __forceinline__ bool k_item(int T, int B, int H, KItem& it) {
+  const int nkb = (T + 31) / 32, nkg = (nkb + AT_WAVES - 1) / AT_WAVES;
+  const int64_t id = blockIdx.x;
+  if (id >= (int64_t)nkg * B * H) return false;
+  const int z = (int)(id % (B * H));
+  const int kg = (int)(id / (B * H));
+  it.kb = kg * AT_WAVES + (int)(threadIdx.x >> 6);
+  it.first = kg * AT_WAVES * 32 / AT_STEP;
+  it.mine = it.kb * 32 / AT_STEP;
+  it.nst = (T + AT_STEP - 1) / AT_STEP;
+  it.active = it.kb < nkb;
   it.b = z / H;
   it.hh = z % H;
   return true;
 }
 
-// Zero 4-key groups [kbeg, kend) of one row of a [T][T] bf16 matrix (this
-// lane's half of every 8-key group).
-__device__ __forceinline__ void zero_row(bf16_t* row, int kbeg, int kend, int h) {
-  for (int k = kbeg + 4 * h; k < kend; k += 8) *reinterpret_cast<u32x2*>(row + k) = u32x2{0u, 0u};
+// Store a 32 x DH accumulator block held transposed (lane: row of the
+// output, registers: columns db*32 + acc_key(r, h)) as bfloat16 (and
+// optionally float32) with 8-byte (16-byte) segments.
+template <int DB>
+__device__ __forceinline__ void store_rows(const f32x16 (&acc)[DB], float mul, bf16_t* out16, float* out32,
+                                           int h) {
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int c = db * 32 + g * 8 + 4 * h;
+      const float a0 = acc[db][4 * g] * mul, a1 = acc[db][4 * g + 1] * mul;
+      const float a2 = acc[db][4 * g + 2] * mul, a3 = acc[db][4 * g + 3] * mul;
+      *reinterpret_cast<u32x2*>(out16 + c) = u32x2{pack_bf2(a0, a1), pack_bf2(a2, a3)};
+      if (out32) *reinterpret_cast<f32x4*>(out32 + c) = f32x4{a0, a1, a2, a3};
+    }
+  }
 }
 
-// Forward.  Exponentials are taken base 2 on scores pre-multiplied by
-// scale * log2(e) (the hardware exp2); P is rounded to bfloat16 after
-// normalisation.  While a tile is used, the workgroup fetches the next one.
+// ---- forward
 template <int DH>
 __global__ __launch_bounds__(AT_THREADS) void attn_fwd_kernel(const bf16_t* __restrict__ qkv,
-                                                              bf16_t* __restrict__ P,
                                                               bf16_t* __restrict__ O,
-                                                              float* __restrict__ Of, int B, int H,
+                                                              float* __restrict__ Of,
+                                                              float* __restrict__ lse, int B, int H,
                                                               int T, float scale) {
-  constexpr int KS = DH / 16, DB = DH / 32, TB = 32 * DH * 2;
+  constexpr int KS = DH / 16, DB = DH / 32, TB = AT_STEP * DH * 2;
   __shared__ __attribute__((aligned(1024))) char kbuf[2][TB];
   __shared__ __attribute__((aligned(1024))) char vbuf[2][TB];
-  Item it;
-  if (!item_of(T, B, H, it)) return;
+  QItem it;
+  if (!q_item(T, B, H, it)) return;
   const int lane = threadIdx.x & 63;
   const int h = lane >> 5, col = lane & 31;
   const int d = H * DH;
@@ -188,150 +242,125 @@ __global__ __launch_bounds__(AT_THREADS) void attn_fwd_kernel(const bf16_t* __re
   const bf16_t* Qp = qkv + (int64_t)it.b * T * ld + it.hh * DH;
   const bf16_t* Kp = Qp + d;
   const bf16_t* Vp = Qp + 2 * d;
-  const int q = it.qb * 32 + col, qc = min(q, T - 1);
+  const int qlo = it.qb * 32, q = qlo + col, qc = min(q, T - 1);
   const float c2 = scale * 1.4426950408889634f;  // scale * log2(e)
   bf16x8 qf[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(Qp + qc * ld + 16 * ks + 8 * h);
-  auto valid = [&](int key) { return key <= q && key < T; };
-  auto scores = [&](const char* kt_lds) {
-    f32x16 acc;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kt_lds, ks, lane), qf[ks], acc, 0, 0, 0);
-    return acc;
-  };
-  Stage<DH> sk, sv;
-  // pass 1: row maximum and sum of exponentials over this lane's keys
-  float mx = -INFINITY, sm = 0.f;
-  fetch<DH>(sk, Kp, ld, 0, T);
-  put<DH, false>(sk, kbuf[0]);
-  tile_barrier();
-  for (int kt = 0; kt < it.nkt; ++kt) {
-    if (kt + 1 < it.nkt) fetch<DH>(sk, Kp, ld, (kt + 1) * 32, T);
-    if (kt < it.mine) {
-      const f32x16 s = scores(kbuf[kt & 1]);
-      float tmax = -INFINITY;
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (valid(kt * 32 + acc_key(r, h))) tmax = fmaxf(tmax, s[r] * c2);
-      if (tmax > -INFINITY) {
-        const float mn = fmaxf(mx, tmax);
-        float acc = (mx > -INFINITY) ? sm * __builtin_amdgcn_exp2f(mx - mn) : 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (valid(kt * 32 + acc_key(r, h))) acc += __builtin_amdgcn_exp2f(fmaf(s[r], c2, -mn));
-        sm = acc;
-        mx = mn;
-      }
-    }
-    if (kt + 1 < it.nkt) put<DH, false>(sk, kbuf[(kt + 1) & 1]);
-    tile_barrier();
-  }
-  // combine the two lane halves of the query
-  const float mo = __shfl_xor(mx, 32, 64), so = __shfl_xor(sm, 32, 64);
-  const float m = fmaxf(mx, mo);
-  const float l = ((mx > -INFINITY) ? sm * __builtin_amdgcn_exp2f(mx - m) : 0.f) +
-                  ((mo > -INFINITY) ? so * __builtin_amdgcn_exp2f(mo - m) : 0.f);
-  const float inv = 1.0f / l;
-  // pass 2: normalised P (stored), O^T += V^T P^T
   f32x16 oacc[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
-  const int64_t z = (int64_t)it.b * H + it.hh;
-  bf16_t* Prow = P + (z * T + qc) * (int64_t)T;
-  fetch<DH>(sk, Kp, ld, 0, T);
-  fetch<DH>(sv, Vp, ld, 0, T);
-  put<DH, false>(sk, kbuf[0]);
-  put<DH, true>(sv, vbuf[0]);
-  tile_barrier();
-  for (int kt = 0; kt < it.nkt; ++kt) {
-    if (kt + 1 < it.nkt) {
-      fetch<DH>(sk, Kp, ld, (kt + 1) * 32, T);
-      fetch<DH>(sv, Vp, ld, (kt + 1) * 32, T);
+  // running maximum (shared by the two lane halves of a query) and this
+  // lane's partial sum; the first key of every computed step is <= q, so
+  // the maximum is finite after the first step
+  float m = -INFINITY, l = 0.f;
+  Stage<DH, AT_STEP> sk, sv;
+  fetch<DH, AT_STEP>(sk, Kp, ld, 0, T);
+  fetch<DH, AT_STEP>(sv, Vp, ld, 0, T);
+  put<DH, AT_STEP, false>(sk, kbuf[0]);
+  put<DH, AT_STEP, true>(sv, vbuf[0]);
+  loop_entry_barrier();
+  for (int st = 0; st < it.nst; ++st) {
+    if (st + 1 < it.nst) {
+      fetch<DH, AT_STEP>(sk, Kp, ld, (st + 1) * AT_STEP, T);
+      fetch<DH, AT_STEP>(sv, Vp, ld, (st + 1) * AT_STEP, T);
     }
-    if (kt < it.mine) {
-      const f32x16 s = scores(kbuf[kt & 1]);
-      float p[16];
+    if (st < it.mine) {
+      const char* kt = kbuf[st & 1];
+      const char* vt = vbuf[st & 1];
+      f32x16 s0, s1;
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        p[r] = valid(kt * 32 + acc_key(r, h)) ? __builtin_amdgcn_exp2f(fmaf(s[r], c2, -m)) * inv : 0.f;
-      const bf16x8 pb0 = pack8(p), pb1 = pack8(p + 8);
-      const char* vt = vbuf[kt & 1];
+      for (int r = 0; r < 16; ++r) s0[r] = s1[r] = 0.f;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(vt, db * 32, 0, lane), pb0, oacc[db], 0, 0, 0);
-        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(vt, db * 32, 1, lane), pb1, oacc[db], 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks) {
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kt, 0, ks, lane), qf[ks], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kt, 1, ks, lane), qf[ks], s1, 0, 0, 0);
       }
-      if (q < T) {
+      const int k0 = st * AT_STEP;
+      float x[32];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int key = kt * 32 + g * 8 + 4 * h;
-          if (key < T) {
-            u32x2 w;
-            w[0] = pack_bf2(p[4 * g], p[4 * g + 1]);
-            w[1] = pack_bf2(p[4 * g + 2], p[4 * g + 3]);
-            *reinterpret_cast<u32x2*>(Prow + key) = w;
-          }
+      for (int r = 0; r < 16; ++r) {
+        x[r] = s0[r] * c2;
+        x[16 + r] = s1[r] * c2;
+      }
+      if (k0 + AT_STEP - 1 > qlo || k0 + AT_STEP > T) {  // diagonal or last step: mask
+#pragma unroll
+        for (int r = 0; r < 32; ++r) {
+          const int key = k0 + 32 * (r >> 4) + acc_key(r & 15, h);
+          if (!(key <= q && key < T)) x[r] = -INFINITY;
         }
       }
+      float tmax = x[0];
+#pragma unroll
+      for (int r = 1; r < 32; ++r) tmax = fmaxf(tmax, x[r]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float mn = fmaxf(m, tmax);
+      const float alpha = __builtin_amdgcn_exp2f(m - mn);  // 0 on the first step
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 32; ++r) {
+        x[r] = __builtin_amdgcn_exp2f(x[r] - mn);
+        ps += x[r];
+      }
+      l = fmaf(l, alpha, ps);
+      m = mn;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[db][r] *= alpha;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) pb[k] = pack8(x + 8 * k);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(vt, db * 32, k, lane), pb[k], oacc[db], 0, 0, 0);
     }
-    if (kt + 1 < it.nkt) {
-      put<DH, false>(sk, kbuf[(kt + 1) & 1]);
-      put<DH, true>(sv, vbuf[(kt + 1) & 1]);
+    if (st + 1 < it.nst) {
+      put<DH, AT_STEP, false>(sk, kbuf[(st + 1) & 1]);
+      put<DH, AT_STEP, true>(sv, vbuf[(st + 1) & 1]);
     }
     tile_barrier();
   }
   if (q >= T) return;
-  // zeros above the diagonal up to the end of the query's 128-row band
-  zero_row(Prow, it.mine * 32, min(T, (it.qb * 32 / AT_ZERO_BAND + 1) * AT_ZERO_BAND), h);
-  // O (bf16) and its float32 copy: lane holds query q, columns db*32 + acc_key(r, h)
+  const float lt = l + __shfl_xor(l, 32, 64);
   const int64_t orow = ((int64_t)it.b * T + q) * d + it.hh * DH;
-#pragma unroll
-  for (int db = 0; db < DB; ++db) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int c = db * 32 + g * 8 + 4 * h;
-      u32x2 w;
-      w[0] = pack_bf2(oacc[db][4 * g], oacc[db][4 * g + 1]);
-      w[1] = pack_bf2(oacc[db][4 * g + 2], oacc[db][4 * g + 3]);
-      *reinterpret_cast<u32x2*>(O + orow + c) = w;
-      f32x4 f = {oacc[db][4 * g], oacc[db][4 * g + 1], oacc[db][4 * g + 2], oacc[db][4 * g + 3]};
-      *reinterpret_cast<f32x4*>(Of + orow + c) = f;
-    }
-  }
+  store_rows<DB>(oacc, 1.0f / lt, O + orow, Of + orow, h);
+  if (h == 0) lse[((int64_t)it.b * H + it.hh) * T + q] = m + log2f(lt);
 }
 
-// Backward: dS and dQ, with the same workgroup structure: V tiles (row read,
-// for dP^T = V dO^T) and K tiles (transposed read, for dQ^T = K^T dS^T) are
-// shared through LDS; each wave reads its own rows of P.
+// ---- backward (1): dQ and D, per block of queries
 template <int DH>
-__global__ __launch_bounds__(AT_THREADS) void attn_bwd_kernel(
-    const bf16_t* __restrict__ qkv, const bf16_t* __restrict__ P, const bf16_t* __restrict__ dO,
-    const float* __restrict__ Of, bf16_t* __restrict__ dS, bf16_t* __restrict__ dQ, int B, int H,
+__global__ __launch_bounds__(AT_THREADS) void attn_bwd_dq_kernel(
+    const bf16_t* __restrict__ qkv, const float* __restrict__ lse, const bf16_t* __restrict__ dO,
+    const float* __restrict__ Of, float* __restrict__ Dout, bf16_t* __restrict__ dqkv, int B, int H,
     int T, float scale) {
-  constexpr int KS = DH / 16, DB = DH / 32, TB = 32 * DH * 2;
-  __shared__ __attribute__((aligned(1024))) char kbuf[2][TB];
-  __shared__ __attribute__((aligned(1024))) char vbuf[2][TB];
-  Item it;
-  if (!item_of(T, B, H, it)) return;
+  constexpr int KS = DH / 16, DB = DH / 32, TB = AT_STEP * DH * 2;
+  __shared__ __attribute__((aligned(1024))) char krow[2][TB];
+  __shared__ __attribute__((aligned(1024))) char ktr[2][TB];
+  __shared__ __attribute__((aligned(1024))) char vrow[2][TB];
+  QItem it;
+  if (!q_item(T, B, H, it)) return;
   const int lane = threadIdx.x & 63;
   const int h = lane >> 5, col = lane & 31;
   const int d = H * DH;
   const int64_t ld = 3 * (int64_t)d;
-  const bf16_t* Kp = qkv + (int64_t)it.b * T * ld + d + it.hh * DH;
-  const bf16_t* Vp = Kp + d;
-  const int q = it.qb * 32 + col, qc = min(q, T - 1);
+  const bf16_t* Qp = qkv + (int64_t)it.b * T * ld + it.hh * DH;
+  const bf16_t* Kp = Qp + d;
+  const bf16_t* Vp = Qp + 2 * d;
+  const int qlo = it.qb * 32, q = qlo + col, qc = min(q, T - 1);
+  const float c2 = scale * 1.4426950408889634f;
+  const int64_t z = (int64_t)it.b * H + it.hh;
   const int64_t orow = ((int64_t)it.b * T + qc) * d + it.hh * DH;
-  // dO^T operand and rowsum(dP * P) = dO . O (this lane's half of the columns)
-  bf16x8 df[KS];
+  // Q^T and dO^T operands; D = dO . O over this lane's half of the columns
+  bf16x8 qf[KS], df[KS];
   float part = 0.f;
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
+    qf[ks] = *reinterpret_cast<const bf16x8*>(Qp + qc * ld + 16 * ks + 8 * h);
     df[ks] = *reinterpret_cast<const bf16x8*>(dO + orow + 16 * ks + 8 * h);
     const f32x4 o0 = *reinterpret_cast<const f32x4*>(Of + orow + 16 * ks + 8 * h);
     const f32x4 o1 = *reinterpret_cast<const f32x4*>(Of + orow + 16 * ks + 8 * h + 4);
@@ -345,123 +374,223 @@ __global__ __launch_bounds__(AT_THREADS) void attn_bwd_kernel(
     }
   }
   const float D = part + __shfl_xor(part, 32, 64);
-  const int64_t z = (int64_t)it.b * H + it.hh;
-  const bf16_t* Prow = P + (z * T + qc) * (int64_t)T;
-  bf16_t* dSrow = dS + (z * T + qc) * (int64_t)T;
+  const float ls = lse[z * T + qc];
+  if (q < T && h == 0 && it.mine > 0) Dout[z * T + q] = D;
   f32x16 qacc[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) qacc[i][r] = 0.f;
-  auto load_p = [&](u32x2 (&pw)[4], int kt) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-      pw[g] = *reinterpret_cast<const u32x2*>(Prow + min(kt * 32 + g * 8 + 4 * h, T - 4));
-  };
-  u32x2 pw[4];
-  Stage<DH> sk, sv;
-  if (it.mine > 0) load_p(pw, 0);
-  fetch<DH>(sk, Kp, ld, 0, T);
-  fetch<DH>(sv, Vp, ld, 0, T);
-  put<DH, true>(sk, kbuf[0]);
-  put<DH, false>(sv, vbuf[0]);
-  tile_barrier();
-  for (int kt = 0; kt < it.nkt; ++kt) {
-    if (kt + 1 < it.nkt) {
-      fetch<DH>(sk, Kp, ld, (kt + 1) * 32, T);
-      fetch<DH>(sv, Vp, ld, (kt + 1) * 32, T);
+  Stage<DH, AT_STEP> sk, sv;
+  fetch<DH, AT_STEP>(sk, Kp, ld, 0, T);
+  fetch<DH, AT_STEP>(sv, Vp, ld, 0, T);
+  put<DH, AT_STEP, false>(sk, krow[0]);
+  put<DH, AT_STEP, true>(sk, ktr[0]);
+  put<DH, AT_STEP, false>(sv, vrow[0]);
+  loop_entry_barrier();
+  for (int st = 0; st < it.nst; ++st) {
+    if (st + 1 < it.nst) {
+      fetch<DH, AT_STEP>(sk, Kp, ld, (st + 1) * AT_STEP, T);
+      fetch<DH, AT_STEP>(sv, Vp, ld, (st + 1) * AT_STEP, T);
     }
-    if (kt < it.mine) {
-      // dP^T = V dO^T for this tile
-      f32x16 acc;
+    if (st < it.mine) {
+      const char* kr = krow[st & 1];
+      const char* kt = ktr[st & 1];
+      const char* vr = vrow[st & 1];
+      const int k0 = st * AT_STEP;
+      const bool edge = k0 + AT_STEP - 1 > qlo || k0 + AT_STEP > T;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-      const char* vt = vbuf[kt & 1];
+      for (int sub = 0; sub < 2; ++sub) {
+        f32x16 sa, pa;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(vt, ks, lane), df[ks], acc, 0, 0, 0);
-      float ds[16];
+        for (int r = 0; r < 16; ++r) sa[r] = pa[r] = 0.f;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int key = kt * 32 + g * 8 + 4 * h;
-        const float pv[4] = {__builtin_bit_cast(float, pw[g][0] << 16), __builtin_bit_cast(float, pw[g][0] & 0xffff0000u),
-                             __builtin_bit_cast(float, pw[g][1] << 16), __builtin_bit_cast(float, pw[g][1] & 0xffff0000u)};
+        for (int ks = 0; ks < KS; ++ks) {
+          sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kr, sub, ks, lane), qf[ks], sa, 0, 0, 0);
+          pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(vr, sub, ks, lane), df[ks], pa, 0, 0, 0);
+        }
+        float ds[16];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          ds[4 * g + e] = (key + e <= q && key + e < T) ? scale * pv[e] * (acc[4 * g + e] - D) : 0.f;
-      }
-      if (kt + 1 < it.mine) load_p(pw, kt + 1);
-      const bf16x8 sb0 = pack8(ds), sb1 = pack8(ds + 8);
-      const char* ktl = kbuf[kt & 1];
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 32 * sub + acc_key(r, h);
+          // masked entries: exp2(-inf) = 0 (a select, no branch); P at its
+          // bfloat16 storage precision (the value dV = P^T dO uses)
+          const float a = fmaf(sa[r], c2, -ls);
+          const float arg = (!edge | ((key <= q) & (key < T))) ? a : -INFINITY;
+          const float p = bf2f(f2bf(__builtin_amdgcn_exp2f(arg)));
+          ds[r] = scale * p * (pa[r] - D);
+        }
+        const bf16x8 d0 = pack8(ds), d1 = pack8(ds + 8);
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        qacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(ktl, db * 32, 0, lane), sb0, qacc[db], 0, 0, 0);
-        qacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(ktl, db * 32, 1, lane), sb1, qacc[db], 0, 0, 0);
-      }
-      if (q < T) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int key = kt * 32 + g * 8 + 4 * h;
-          if (key < T) {
-            u32x2 w;
-            w[0] = pack_bf2(ds[4 * g], ds[4 * g + 1]);
-            w[1] = pack_bf2(ds[4 * g + 2], ds[4 * g + 3]);
-            *reinterpret_cast<u32x2*>(dSrow + key) = w;
-          }
+        for (int db = 0; db < DB; ++db) {
+          qacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(kt, db * 32, 2 * sub, lane), d0, qacc[db], 0, 0, 0);
+          qacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(kt, db * 32, 2 * sub + 1, lane), d1, qacc[db], 0, 0, 0);
         }
       }
     }
-    if (kt + 1 < it.nkt) {
-      put<DH, true>(sk, kbuf[(kt + 1) & 1]);
-      put<DH, false>(sv, vbuf[(kt + 1) & 1]);
+    if (st + 1 < it.nst) {
+      put<DH, AT_STEP, false>(sk, krow[(st + 1) & 1]);
+      put<DH, AT_STEP, true>(sk, ktr[(st + 1) & 1]);
+      put<DH, AT_STEP, false>(sv, vrow[(st + 1) & 1]);
     }
     tile_barrier();
   }
   if (q >= T) return;
-  zero_row(dSrow, it.mine * 32, min(T, (it.qb * 32 / AT_ZERO_BAND + 1) * AT_ZERO_BAND), h);
-  // dQ (bf16) into the q columns of the dqkv rows
-  const int64_t qrow = ((int64_t)it.b * T + q) * ld + it.hh * DH;
+  store_rows<DB>(qacc, 1.0f, dqkv + ((int64_t)it.b * T + q) * ld + it.hh * DH, nullptr, h);
+}
+
+// ---- backward (2): dK and dV, per block of keys
+template <int DH>
+__global__ __launch_bounds__(AT_THREADS) void attn_bwd_dkv_kernel(
+    const bf16_t* __restrict__ qkv, const float* __restrict__ lse, const bf16_t* __restrict__ dO,
+    const float* __restrict__ Din, bf16_t* __restrict__ dqkv, int B, int H, int T, float scale) {
+  constexpr int KS = DH / 16, DB = DH / 32, TB = AT_STEP * DH * 2;
+  __shared__ __attribute__((aligned(1024))) char qrow[2][TB];
+  __shared__ __attribute__((aligned(1024))) char qtr[2][TB];
+  __shared__ __attribute__((aligned(1024))) char orow_t[2][TB];
+  __shared__ __attribute__((aligned(1024))) char otr[2][TB];
+  __shared__ __attribute__((aligned(16))) float lsd[2][2][AT_STEP];  // [stage][lse, D][query]
+  KItem it;
+  if (!k_item(T, B, H, it)) return;
+  const int lane = threadIdx.x & 63;
+  const int h = lane >> 5, col = lane & 31;
+  const int d = H * DH;
+  const int64_t ld = 3 * (int64_t)d;
+  const bf16_t* Qp = qkv + (int64_t)it.b * T * ld + it.hh * DH;
+  const bf16_t* dOp = dO + (int64_t)it.b * T * d + it.hh * DH;
+  const int64_t z = (int64_t)it.b * H + it.hh;
+  const float* lsep = lse + z * T;
+  const float* Dp = Din + z * T;
+  const int key = it.kb * 32 + col, kc = min(key, T - 1);
+  const float c2 = scale * 1.4426950408889634f;
+  // K^T and V^T operands of this lane's key
+  bf16x8 kf[KS], vf[KS];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int c = db * 32 + g * 8 + 4 * h;
-      u32x2 w;
-      w[0] = pack_bf2(qacc[db][4 * g], qacc[db][4 * g + 1]);
-      w[1] = pack_bf2(qacc[db][4 * g + 2], qacc[db][4 * g + 3]);
-      *reinterpret_cast<u32x2*>(dQ + qrow + c) = w;
-    }
+  for (int ks = 0; ks < KS; ++ks) {
+    kf[ks] = *reinterpret_cast<const bf16x8*>(Qp + kc * ld + d + 16 * ks + 8 * h);
+    vf[ks] = *reinterpret_cast<const bf16x8*>(Qp + kc * ld + 2 * d + 16 * ks + 8 * h);
   }
+  f32x16 kacc[DB], vacc[DB];
+#pragma unroll
+  for (int i = 0; i < DB; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) kacc[i][r] = vacc[i][r] = 0.f;
+  Stage<DH, AT_STEP> sq, so;
+  float sl = 0.f;  // one lse or D value per thread of the first 128
+  auto fetch_l = [&](int q0) {
+    const int t = threadIdx.x;
+    if (t < 2 * AT_STEP) sl = (t < AT_STEP ? lsep : Dp)[min(q0 + (t % AT_STEP), T - 1)];
+  };
+  auto put_l = [&](int stg) {
+    const int t = threadIdx.x;
+    if (t < 2 * AT_STEP) lsd[stg][t / AT_STEP][t % AT_STEP] = sl;
+  };
+  const int q0 = it.first * AT_STEP;
+  fetch<DH, AT_STEP>(sq, Qp, ld, q0, T);
+  fetch<DH, AT_STEP>(so, dOp, d, q0, T);
+  fetch_l(q0);
+  put<DH, AT_STEP, false>(sq, qrow[0]);
+  put<DH, AT_STEP, true>(sq, qtr[0]);
+  put<DH, AT_STEP, false>(so, orow_t[0]);
+  put<DH, AT_STEP, true>(so, otr[0]);
+  put_l(0);
+  loop_entry_barrier();
+  for (int st = it.first; st < it.nst; ++st) {
+    const int stg = (st - it.first) & 1;
+    if (st + 1 < it.nst) {
+      fetch<DH, AT_STEP>(sq, Qp, ld, (st + 1) * AT_STEP, T);
+      fetch<DH, AT_STEP>(so, dOp, d, (st + 1) * AT_STEP, T);
+      fetch_l((st + 1) * AT_STEP);
+    }
+    if (it.active && st >= it.mine) {
+      const int qs = st * AT_STEP;
+      const bool edge = qs < it.kb * 32 + 32 || qs + AT_STEP > T;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+        f32x16 sa, pa;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sa[r] = pa[r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(qrow[stg], sub, ks, lane), kf[ks], sa, 0, 0, 0);
+          pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(orow_t[stg], sub, ks, lane), vf[ks], pa, 0, 0, 0);
+        }
+        float p[16], ds[16];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int qi = 32 * sub + 8 * g + 4 * h;  // query of registers 4g..4g+3, within the step
+          const f32x4 lv = *reinterpret_cast<const f32x4*>(&lsd[stg][0][qi]);
+          const f32x4 dv = *reinterpret_cast<const f32x4*>(&lsd[stg][1][qi]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * g + e, qq = qs + qi + e;
+            const float a = fmaf(sa[r], c2, -lv[e]);
+            const float arg = (!edge | ((qq >= key) & (qq < T))) ? a : -INFINITY;  // masked: exp2 -> 0
+            const float pe = bf2f(f2bf(__builtin_amdgcn_exp2f(arg)));
+            p[r] = pe;
+            ds[r] = scale * pe * (pa[r] - dv[e]);
+          }
+        }
+        const bf16x8 p0 = pack8(p), p1 = pack8(p + 8), d0 = pack8(ds), d1 = pack8(ds + 8);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[stg], db * 32, 2 * sub, lane), p0, vacc[db], 0, 0, 0);
+          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[stg], db * 32, 2 * sub + 1, lane), p1, vacc[db], 0, 0, 0);
+          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[stg], db * 32, 2 * sub, lane), d0, kacc[db], 0, 0, 0);
+          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[stg], db * 32, 2 * sub + 1, lane), d1, kacc[db], 0, 0, 0);
+        }
+      }
+    }
+    if (st + 1 < it.nst) {
+      put<DH, AT_STEP, false>(sq, qrow[stg ^ 1]);
+      put<DH, AT_STEP, true>(sq, qtr[stg ^ 1]);
+      put<DH, AT_STEP, false>(so, orow_t[stg ^ 1]);
+      put<DH, AT_STEP, true>(so, otr[stg ^ 1]);
+      put_l(stg ^ 1);
+    }
+    tile_barrier();
+  }
+  if (!it.active || key >= T) return;
+  bf16_t* rowp = dqkv + ((int64_t)it.b * T + key) * ld + it.hh * DH;
+  store_rows<DB>(kacc, 1.0f, rowp + d, nullptr, h);
+  store_rows<DB>(vacc, 1.0f, rowp + 2 * d, nullptr, h);
 }
 
 }  // namespace
 
 bool attention_fused_supported(int dh) { return dh == 32 || dh == 64 || dh == 128; }
 
-hipError_t launch_attention_fwd(const bf16_t* qkv, bf16_t* P, bf16_t* O, float* Of, int B, int H,
+hipError_t launch_attention_fwd(const bf16_t* qkv, float* lse, bf16_t* O, float* Of, int B, int H,
                                 int T, int dh, float scale, hipStream_t s) {
-  if (T % 8) return hipErrorInvalidValue;
-  const int64_t groups = cdiv(cdiv(T, 32), AT_WAVES) * B * H;
-  const dim3 grid((unsigned)groups);
+  if (T % 8 || T <= 0) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(cdiv(cdiv(T, 32), AT_WAVES) * B * H));
   switch (dh) {
-    case 32: attn_fwd_kernel<32><<<grid, AT_THREADS, 0, s>>>(qkv, P, O, Of, B, H, T, scale); break;
-    case 64: attn_fwd_kernel<64><<<grid, AT_THREADS, 0, s>>>(qkv, P, O, Of, B, H, T, scale); break;
-    case 128: attn_fwd_kernel<128><<<grid, AT_THREADS, 0, s>>>(qkv, P, O, Of, B, H, T, scale); break;
+    case 32: attn_fwd_kernel<32><<<grid, AT_THREADS, 0, s>>>(qkv, O, Of, lse, B, H, T, scale); break;
+    case 64: attn_fwd_kernel<64><<<grid, AT_THREADS, 0, s>>>(qkv, O, Of, lse, B, H, T, scale); break;
+    case 128: attn_fwd_kernel<128><<<grid, AT_THREADS, 0, s>>>(qkv, O, Of, lse, B, H, T, scale); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attention_bwd(const bf16_t* qkv, const bf16_t* P, const bf16_t* dO, const float* Of,
-                                bf16_t* dS, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
+hipError_t launch_attention_bwd(const bf16_t* qkv, const float* lse, const bf16_t* dO, const float* Of,
+                                float* D, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
                                 hipStream_t s) {
-  if (T % 8) return hipErrorInvalidValue;
-  const int64_t groups = cdiv(cdiv(T, 32), AT_WAVES) * B * H;
-  const dim3 grid((unsigned)groups);
+  if (T % 8 || T <= 0) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(cdiv(cdiv(T, 32), AT_WAVES) * B * H));
   switch (dh) {
-    case 32: attn_bwd_kernel<32><<<grid, AT_THREADS, 0, s>>>(qkv, P, dO, Of, dS, dqkv, B, H, T, scale); break;
-    case 64: attn_bwd_kernel<64><<<grid, AT_THREADS, 0, s>>>(qkv, P, dO, Of, dS, dqkv, B, H, T, scale); break;
-    case 128: attn_bwd_kernel<128><<<grid, AT_THREADS, 0, s>>>(qkv, P, dO, Of, dS, dqkv, B, H, T, scale); break;
+    case 32:
+      attn_bwd_dq_kernel<32><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, Of, D, dqkv, B, H, T, scale);
+      attn_bwd_dkv_kernel<32><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, D, dqkv, B, H, T, scale);
+      break;
+    case 64:
+      attn_bwd_dq_kernel<64><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, Of, D, dqkv, B, H, T, scale);
+      attn_bwd_dkv_kernel<64><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, D, dqkv, B, H, T, scale);
+      break;
+    case 128:
+      attn_bwd_dq_kernel<128><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, Of, D, dqkv, B, H, T, scale);
+      attn_bwd_dkv_kernel<128><<<grid, AT_THREADS, 0, s>>>(qkv, lse, dO, D, dqkv, B, H, T, scale);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -333,9 +333,11 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
     // stage that was read in the previous step (every wave has waited for
     // its reads of that stage before its last MFMAs)
     const int younger = min(STAGES - 2, nk - 1 - kt);
-    if (younger >= 2) WAIT_VMCNT(2 * LOADS);
-    else if (younger == 1) WAIT_VMCNT(LOADS);
-    else WAIT_VMCNT(0);
+    static_for<0, STAGES - 1>([&](auto Y) {
+      constexpr int y = decltype(Y)::value;
+      static_assert(y * LOADS <= 63, "vmcnt field");
+      if (younger == y) WAIT_VMCNT(y * LOADS);
+    });
     barrier_only();
     char* st = smem + (kt % STAGES) * STAGE;
     if (kt == nk - 1 && krem < BKV) {

@@ -176,13 +176,16 @@ hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, f
                               hipStream_t s);
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,
                               float scale, hipStream_t s);
-// Fused causal attention (head width 32, 64 or 128): P, O (bf16) and the
-// float32 O from qkv; dS and dQ from qkv, P, dO and the float32 O.
+// Fused causal attention (head width 32, 64 or 128).  Forward: O (bf16),
+// O in float32 and the base-2 log-sum-exp of each query's scaled scores
+// (lse, [B][H][T]) from qkv.  Backward: dQ, dK, dV into the q, k, v columns
+// of dqkv from qkv, lse, dO and the float32 O; D ([B][H][T]) receives
+// rowsum(dP P) = dO . O.
 bool attention_fused_supported(int dh);
-hipError_t launch_attention_fwd(const bf16_t* qkv, bf16_t* P, bf16_t* O, float* Of, int B, int H,
+hipError_t launch_attention_fwd(const bf16_t* qkv, float* lse, bf16_t* O, float* Of, int B, int H,
                                 int T, int dh, float scale, hipStream_t s);
-hipError_t launch_attention_bwd(const bf16_t* qkv, const bf16_t* P, const bf16_t* dO, const float* Of,
-                                bf16_t* dS, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
+hipError_t launch_attention_bwd(const bf16_t* qkv, const float* lse, const bf16_t* dO, const float* Of,
+                                float* D, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
                                 hipStream_t s);
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B,
                              int T, int V, bf16_t* dlogits, float* loss_rows, float* loss_out,

@@ -130,8 +130,9 @@ struct Carver {
 
 struct BlockActs {
   float *x, *h, *mean1, *rstd1, *mean2, *rstd2;
-  bf16_t *a, *qkv, *P, *o, *a2, *f, *gl;
-  float* of;  // float32 attention output (fused attention: rowsum(dP P) = dO . O)
+  bf16_t *a, *qkv, *P, *o, *a2, *f, *gl;  // P: softmax probabilities (unfused attention only)
+  float* of;   // fused attention: float32 O (rowsum(dP P) = dO . O in the backward)
+  float* lse;  // fused attention: base-2 log-sum-exp of each query's scaled scores
 };
 
 // Fused attention kernels cover head widths 32, 64 and 128; other widths use
@@ -180,7 +181,8 @@ struct layup_ctx {
   float* loss_rows = nullptr;
   uint32_t* sorted = nullptr;
   float* S = nullptr;       // scores, then dP
-  bf16_t* dS = nullptr;
+  bf16_t* dS = nullptr;      // unfused attention: score gradient
+  float* att_D = nullptr;    // fused attention: rowsum(dP P) per query
   float* dx[2] = {nullptr, nullptr};
   float* dh = nullptr;
   float* da = nullptr;
@@ -221,12 +223,13 @@ size_t carve(layup_ctx* c, char* base) {
       A.rstd2 = cv.take<float>(N);
       A.a = cv.take<bf16_t>(N * d);
       A.qkv = cv.take<bf16_t>(N * 3 * d);
-      A.P = cv.take<bf16_t>(g.batch * H * T * T);
+      A.P = fused ? nullptr : cv.take<bf16_t>(g.batch * H * T * T);
       A.o = cv.take<bf16_t>(N * d);
       A.a2 = cv.take<bf16_t>(N * d);
       A.f = cv.take<bf16_t>(N * F);
       A.gl = cv.take<bf16_t>(N * F);
       A.of = fused ? cv.take<float>(N * d) : nullptr;
+      A.lse = fused ? cv.take<float>(g.batch * H * T) : nullptr;
     }
     c->xL = cv.take<float>(N * d);
     c->meanf = cv.take<float>(N);
@@ -236,7 +239,8 @@ size_t carve(layup_ctx* c, char* base) {
     c->loss_rows = cv.take<float>(N);
     c->sorted = cv.take<uint32_t>(N);
     c->S = fused ? nullptr : cv.take<float>(g.batch * H * T * T);
-    c->dS = cv.take<bf16_t>(g.batch * H * T * T);
+    c->dS = fused ? nullptr : cv.take<bf16_t>(g.batch * H * T * T);
+    c->att_D = fused ? cv.take<float>(g.batch * H * T) : nullptr;
     c->dx[0] = cv.take<float>(N * d);
     c->dx[1] = cv.take<float>(N * d);
     c->dh = cv.take<float>(N * d);
@@ -386,7 +390,7 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
     q.bias = fl.p(p + "qkv.b");
     TRY(run_gemm(c, q, s, "qkv forward"));
     if (A.of) {
-      HIPCHK(c, launch_attention_fwd(A.qkv, A.P, A.o, A.of, (int)B, (int)H, (int)T, (int)dh, scale, s),
+      HIPCHK(c, launch_attention_fwd(A.qkv, A.lse, A.o, A.of, (int)B, (int)H, (int)T, (int)dh, scale, s),
              "attention");
     } else {
     // scores S[z] = Q_h K_h^T, z = b*H + h
@@ -497,42 +501,41 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                           p + "proj.w"), s, "proj dW", true));
   HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "proj.b"), s), "proj db");
   if (!fz) TRY(run_gemm(c, prx, s, "proj dX", true));
-  // attention core, batched over z = b*H + h
-  auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
-                     int64_t ci, int causal) {
-    gm.causal = causal;
-    gm.batch = (int)(B * H);
-    gm.inner = (int)H;
-    gm.a_outer = ao;
-    gm.a_inner = ai;
-    gm.b_outer = bo;
-    gm.b_inner = bi;
-    gm.c_outer = co;
-    gm.c_inner = ci;
-    return gm;
-  };
-  const int64_t TT = T * T;
-  if (!A.of) {
-  // dP = dO_h V_h^T
-  TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
-                          T * d, dh, T * 3 * d, dh, H * TT, TT, CAUSAL_OUT_LOWER), s, "dP"));
-  }
-  // dV_h = P^T dO_h
-  TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
-                             EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dV"));
   if (A.of) {
-    // dS and dQ_h = dS K_h in one pass (dP stays in registers)
-    HIPCHK(c, launch_attention_bwd(A.qkv, A.P, c->do16, A.of, c->dS, c->dqkv16, (int)B, (int)H, (int)T,
-                                   (int)dh, scale, s), "attention backward");
+    // attention core, fused: dQ, dK, dV from recomputed scores (P and dS stay
+    // in registers)
+    HIPCHK(c, launch_attention_bwd(A.qkv, A.lse, c->do16, A.of, c->att_D, c->dqkv16, (int)B, (int)H,
+                                   (int)T, (int)dh, scale, s), "attention backward");
   } else {
-  HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
-  // dQ_h = dS K_h
-  TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
-                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_LOWER), s, "dQ"));
+    // attention core, batched over z = b*H + h
+    auto batched = [&](Gemm gm, int64_t ao, int64_t ai, int64_t bo, int64_t bi, int64_t co,
+                       int64_t ci, int causal) {
+      gm.causal = causal;
+      gm.batch = (int)(B * H);
+      gm.inner = (int)H;
+      gm.a_outer = ao;
+      gm.a_inner = ai;
+      gm.b_outer = bo;
+      gm.b_inner = bi;
+      gm.c_outer = co;
+      gm.c_inner = ci;
+      return gm;
+    };
+    const int64_t TT = T * T;
+    // dP = dO_h V_h^T
+    TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
+                            T * d, dh, T * 3 * d, dh, H * TT, TT, CAUSAL_OUT_LOWER), s, "dP"));
+    // dV_h = P^T dO_h
+    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
+                               EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dV"));
+    HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
+    // dQ_h = dS K_h
+    TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
+                               EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_LOWER), s, "dQ"));
+    // dK_h = dS^T Q_h
+    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
+                               EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   }
-  // dK_h = dS^T Q_h
-  TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
-                             EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   // qkv projection
   Gemm qx = mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
   if (fz) TRY(run_gemm(c, qx, s, "qkv dX", true));
@@ -764,7 +767,7 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
     return fail(nullptr, LAYUP_ERR_INVALID_ARG, "workspace smaller than layup_workspace_size");
   }
   c->ws_bytes = carve(c, (char*)workspace);
-  if (cfg->model == LAYUP_MODEL_GPT_BF16) {
+  if (cfg->model == LAYUP_MODEL_GPT_BF16 && !fused_attention(*cfg)) {
     // probabilities and score gradients above the diagonal are zero and no
     // kernel writes them: clear both matrices once
     const size_t pm = (size_t)cfg->batch * cfg->n_head * cfg->seq * cfg->seq * sizeof(bf16_t);
@@ -1067,8 +1070,9 @@ layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, cons
   const layup_config& g = ctx->cfg;
   const int64_t N = (int64_t)g.batch * g.seq, d = g.d_model, F = g.d_ff;
   const int64_t PT = (int64_t)g.batch * g.n_head * g.seq * g.seq;
-  if (which <= 8 && (layer < 0 || layer >= g.n_layer)) return fail(ctx, LAYUP_ERR_INVALID_ARG, "layer out of range");
-  const BlockActs* A = which <= 8 ? &ctx->acts[layer] : nullptr;
+  const bool per_layer = which <= 8 || which == 12;
+  if (per_layer && (layer < 0 || layer >= g.n_layer)) return fail(ctx, LAYUP_ERR_INVALID_ARG, "layer out of range");
+  const BlockActs* A = per_layer ? &ctx->acts[layer] : nullptr;
   const void* p = nullptr;
   int64_t n = 0;
   int dt = 0;
@@ -1076,7 +1080,9 @@ layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, cons
     case 0: p = A->x; n = N * d; dt = 0; break;
     case 1: p = A->a; n = N * d; dt = 1; break;
     case 2: p = A->qkv; n = N * 3 * d; dt = 1; break;
-    case 3: p = A->P; n = PT; dt = 1; break;
+    case 3:
+      if (!A->P) return fail(ctx, LAYUP_ERR_INVALID_ARG, "attention probabilities are not stored by the fused attention (head width 32, 64 or 128); its log-sum-exp is activation 12");
+      p = A->P; n = PT; dt = 1; break;
     case 4: p = A->o; n = N * d; dt = 1; break;
     case 5: p = A->h; n = N * d; dt = 0; break;
     case 6: p = A->a2; n = N * d; dt = 1; break;
@@ -1085,6 +1091,9 @@ layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, cons
     case 9: p = ctx->xf; n = N * d; dt = 1; break;
     case 10: p = ctx->logits; n = N * align64(g.vocab); dt = 1; break;
     case 11: p = ctx->xL; n = N * d; dt = 0; break;
+    case 12:
+      if (!A->lse) return fail(ctx, LAYUP_ERR_INVALID_ARG, "the log-sum-exp is stored by the fused attention only (head width 32, 64 or 128)");
+      p = A->lse; n = (int64_t)g.batch * g.n_head * g.seq; dt = 0; break;
     default: return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown activation");
   }
   *ptr = p;

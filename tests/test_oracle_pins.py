@@ -169,3 +169,22 @@ def test_bf16_special_values():
     # no double rounding: a float64 just above a bfloat16 tie rounds up
     x = 1 + 2 ** -8 + 2 ** -40
     assert O.bf16(A([x]))[0] == 1 + 2 ** -7
+
+
+def test_causal_logsumexp_brute_force_and_softmax():
+    """The causal log-sum-exp (the softmax normaliser the fused attention
+    stores) against a plain loop with math.fsum, and exp(s - lse) against the
+    causal softmax on and below the diagonal; a row whose scores are all
+    equal has lse = s + log(i + 1)."""
+    rng = np.random.default_rng(11)
+    s = rng.normal(0.0, 3.0, (2, 5, 5))
+    lse = O.causal_logsumexp(s)
+    for b in range(2):
+        for i in range(5):
+            want = math.log(math.fsum(math.exp(s[b, i, j]) for j in range(i + 1)))
+            assert abs(lse[b, i] - want) <= 1e-12 * max(1.0, abs(want))
+    p = O.causal_softmax(s)
+    low = np.tril(np.ones((5, 5), dtype=bool))
+    assert np.allclose(np.exp(s - lse[..., None])[:, low], p[:, low], rtol=1e-12, atol=0)
+    flat = np.full((1, 4, 4), 0.7)
+    assert np.allclose(O.causal_logsumexp(flat)[0], 0.7 + np.log(np.arange(1, 5)), rtol=0, atol=1e-14)
