@@ -345,12 +345,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
       zero_tail<BN, BKM, BKV>(st + A_BYTES, krem);
       __syncthreads();
     }
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
     const uint32_t sb = lds0 + (uint32_t)((kt % STAGES) * STAGE);
-    // operand fragments of sub-step ks+1 are read while the MFMAs of ks run
+    // the first sub-step's fragments are requested before the next stage's
+    // copies are issued (their address arithmetic hides the LDS latency);
+    // fragments of sub-step ks+1 are read while the MFMAs of ks run
     u32x4 af[2][TM], bfr[2][TN];
     read_frags<BM, AK, BKV, TM, 0>(sb, a_off, af[0]);
     read_frags<BN, BKM, BKV, TN, 0>(sb, b_off, bfr[0]);
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
     static_for<0, KS>([&](auto KSI) {
       constexpr int ks = decltype(KSI)::value, cb = ks & 1;
       if constexpr (ks + 1 < KS) {
@@ -605,17 +607,17 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
   }
 }
 
-// Tile choice, measured inside the GPT-2-small step (operands arriving from
-// HBM, not repeated launches on cached operands):
+// Tile choice (measured on the GPT-2-small shapes with operands arriving from
+// HBM, as inside the step):
 //  - N <= 64 (attention head width): 128x64;
 //  - both output dimensions >= 2048, K >= 4096 and at least 256 tiles:
 //    256x256 with K steps of 64;
-//  - float32 dX = dY W (k-major A, m-major B) and dW = dY^T X with fewer than
-//    128 tiles: 128x128 with K steps of 64 (fewer waits and barriers);
-//    split-K when the output has fewer than 300 tiles;
-//  - otherwise (forward products, bf16/GELU epilogues, larger dW): 128x128
-//    with K steps of 32 and three stages (more loads in flight for short K);
-//    split-K for float32 outputs with fewer than 512 tiles (dW: 4 splits).
+//  - float32 outputs with an m-major B (dX = dY W, and dW = dY^T X with fewer
+//    than 512 tiles): 128x128 with K steps of 64, two workgroups per CU;
+//    split-K fills the 512 workgroup slots of one round (largest split with
+//    tiles x split <= 512);
+//  - otherwise (forward products, bf16/GELU epilogues): 128x128 with K steps
+//    of 32 and three stages (more loads in flight for short K).
 // Split-K (float32 partials, fixed-order sum) only with K >= 1536, at least
 // 512 K per split, at most 8 splits.
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
@@ -623,17 +625,20 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   auto tiles = [&](int bm, int bn) { return cdiv(g.M, bm) * cdiv(g.N, bn) * g.batch; };
   const bool f32_out = g.epi == EPI_F32 || g.epi == EPI_UPDATE;
   const bool splittable = g.batch == 1 && g.K >= 1536 && f32_out;
+  const int64_t max_split = std::min<int64_t>(8, g.K / 512);
   auto split_for = [&](int64_t t, int64_t want) {
     if (!splittable || t >= want) return 1;
-    return (int)std::min<int64_t>(std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), g.K / 512), 8);
+    return (int)std::min<int64_t>(std::max<int64_t>(2, cdiv(want, t)), max_split);
+  };
+  auto fill_split = [&](int64_t t, int64_t slots) {
+    if (!splittable) return 1;
+    return (int)std::max<int64_t>(1, std::min<int64_t>(slots / t, max_split));
   };
   if (g.N <= 64) return launch_gemm_bf16_cfg(g, 2, 1, s);
   if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256)
     return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
   const int64_t t = tiles(128, 128);
-  if (f32_out && !g.b_kmajor && (g.a_kmajor || t < 128))
-    return launch_gemm_bf16_cfg(g, 3, split_for(t, 300), s);
-  if (!g.a_kmajor) return launch_gemm_bf16_cfg(g, 1, splittable && t < 512 ? 4 : 1, s);
+  if (f32_out && !g.b_kmajor && (g.a_kmajor || t < 512)) return launch_gemm_bf16_cfg(g, 3, fill_split(t, 512), s);
   return launch_gemm_bf16_cfg(g, 1, split_for(t, 512), s);
 }
 
