@@ -581,8 +581,10 @@ static const TileShape kShapes[] = {
     {128, 128},  // 1: 2x4 waves (each 64x32),  3 stages of K 32, 3/CU  (24 waves/CU)
     {128, 64},   // 2: 2x2 waves (each 64x32),  4 stages of K 32, 3/CU  (12 waves/CU)
     {128, 128},  // 3: 2x4 waves (each 64x32),  2 stages of K 64, 2/CU  (16 waves/CU)
+    {256, 256},  // 4: 4x2 waves (each 64x128), 4 stages of K 32, 1/CU  (8 waves/CU)
+    {256, 128},  // 5: 4x2 waves (each 64x64),  3 stages of K 32, 1/CU  (8 waves/CU)
 };
-constexpr int kNumCfg = 4;
+constexpr int kNumCfg = 6;
 
 hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t s) {
   if (g.M == 0 || g.N == 0) return hipSuccess;
@@ -603,6 +605,8 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
     case 0: return dispatch_epi<256, 256, 4, 2, 2, 1, 64>(g, P, s);
     case 1: return dispatch_epi<128, 128, 2, 4, 3, 3, 32>(g, P, s);
     case 2: return dispatch_epi<128, 64, 2, 2, 4, 3, 32>(g, P, s);
+    case 4: return dispatch_epi<256, 256, 4, 2, 4, 1, 32>(g, P, s);
+    case 5: return dispatch_epi<256, 128, 4, 2, 3, 1, 32>(g, P, s);
     default: return dispatch_epi<128, 128, 2, 4, 2, 2, 64>(g, P, s);
   }
 }
@@ -612,12 +616,15 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
 //  - N <= 64 (attention head width): 128x64;
 //  - both output dimensions >= 2048, K >= 4096 and at least 256 tiles:
 //    256x256 with K steps of 64;
+//  - float32 output and K >= 16384 (the tied head's dX over the vocabulary):
+//    256x256 with four stages of K 32 and an 8-way split of K;
 //  - float32 outputs with an m-major B (dX = dY W, and dW = dY^T X with fewer
-//    than 512 tiles): 128x128 with K steps of 64, two workgroups per CU;
-//    split-K fills the 512 workgroup slots of one round (largest split with
-//    tiles x split <= 512);
-//  - otherwise (forward products, bf16/GELU epilogues): 128x128 with K steps
-//    of 32 and three stages (more loads in flight for short K).
+//    than 512 tiles) and float32 forward products: 128x128 with K steps of
+//    64, two workgroups per CU; for m-major B, split-K fills the 512
+//    workgroup slots of one round (largest split with tiles x split <= 512);
+//  - dW with at least 512 tiles (the head's dW): 256x128, three stages of K 32;
+//  - otherwise (forward products with bf16/GELU epilogues): 128x128 with K
+//    steps of 32 and three stages (more loads in flight for short K).
 // Split-K (float32 partials, fixed-order sum) only with K >= 1536, at least
 // 512 K per split, at most 8 splits.
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
@@ -637,8 +644,11 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.N <= 64) return launch_gemm_bf16_cfg(g, 2, 1, s);
   if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256)
     return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
+  if (splittable && g.K >= 16384 && g.a_kmajor) return launch_gemm_bf16_cfg(g, 4, (int)max_split, s);
   const int64_t t = tiles(128, 128);
   if (f32_out && !g.b_kmajor && (g.a_kmajor || t < 512)) return launch_gemm_bf16_cfg(g, 3, fill_split(t, 512), s);
+  if (f32_out && g.a_kmajor && g.b_kmajor) return launch_gemm_bf16_cfg(g, 3, 1, s);
+  if (f32_out && !g.a_kmajor && !g.b_kmajor) return launch_gemm_bf16_cfg(g, 5, 1, s);
   return launch_gemm_bf16_cfg(g, 1, split_for(t, 512), s);
 }
 

@@ -151,7 +151,8 @@ enum Causal : int { CAUSAL_NONE = 0, CAUSAL_OUT_LOWER = 1, CAUSAL_A_LOWER = 2, C
 // Validates shapes/alignment; returns a message or empty string.
 std::string gemm_check(const Gemm& g, bool f32_operands);
 hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t stream);
-// explicit tile configuration (0 = 256x256 K64, 1 = 128x128 K32, 2 = 128x64 K32, 3 = 128x128 K64)
+// explicit tile configuration (0 = 256x256 K64, 1 = 128x128 K32, 2 = 128x64 K32, 3 = 128x128 K64,
+// 4 = 256x256 K32 four stages, 5 = 256x128 K32)
 hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t stream);
 hipError_t launch_gemm_f32(const Gemm& g, hipStream_t stream);
 

@@ -203,7 +203,7 @@ struct layup_ctx {
 
 namespace {
 
-constexpr size_t SPLITK_BYTES = 64u << 20;
+constexpr size_t SPLITK_BYTES = 256u << 20;  // room for an 8-way split of an 8192 x 768 float32 output
 
 size_t carve(layup_ctx* c, char* base) {
   Carver cv{base};

@@ -76,6 +76,26 @@ def test_gemm_split_k_deterministic(layout):
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("layout", ["kn", "kk"])
+def test_gemm_long_k_split(layout):
+    """K >= 16384 with a float32 output (the tied head's dX over the
+    vocabulary) takes the 256x256 tile with an 8-way split of K; ragged M, N
+    and K, reproducible bit for bit."""
+    a, ref = run(layout, 520, 264, 16400, ws=True, seed=13)
+    b, _ = run(layout, 520, 264, 16400, ws=True, seed=13)
+    compare(a, ref, 2e-2, "long-K split")
+    assert np.linalg.norm(a - ref) <= 1e-4 * np.linalg.norm(ref)
+    assert np.array_equal(a, b)
+
+
+def test_gemm_dw_many_tiles():
+    """dW = dY^T X with at least 512 output tiles (the head's dW) takes the
+    256x128 tile; ragged N and K."""
+    got, ref = run("mn", 4096, 2200, 200, seed=17)
+    compare(got, ref, 2e-2, "dW many tiles")
+    assert np.linalg.norm(got - ref) <= 1e-4 * np.linalg.norm(ref)
+
+
 def test_gemm_batched_attention_strides():
     """Batched products over z = b*H + h with two-level operand offsets, as the
     attention core uses them: S_z = Q_h K_h^T from a packed qkv matrix."""
@@ -102,6 +122,8 @@ def test_gemm_batched_attention_strides():
     (768, 3072, 8192, "mn"),    # mlp-proj dW
     (768, 768, 8192, "mn"),     # attn-proj dW
     (8192, 2304, 768, "kk"),    # qkv forward
+    (1024, 768, 50304, "kn"),   # head dX over the vocabulary (1024 of the 8192 rows)
+    (50304, 768, 1024, "mn"),   # head dW (K = 1024 of the 8192 tokens)
 ])
 def test_gemm_full_size_sampled(M, N, K, layout):
     """Full GPT-2-small backward shapes (batch 8 x 1024 tokens), checked on
