@@ -60,11 +60,12 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
 }
 
 // ------------------------------------------------------------ pipeline
-// K advances in steps of BKV (32) through a ring of STAGES (4) LDS stages.  Every
+// K advances in steps of BKV (32 or 64) through rings of LDS stages (one for
+// the A tiles, one for the B tiles; A may run one stage deeper).  Every
 // operand tile is copied HBM -> LDS by direct-to-LDS loads
 // (global_load_lds_dwordx4: each lane's 16 bytes land at LDS base + 16*lane,
 // one 1 KB block per wave instruction), so no registers stage the data and
-// STAGES-1 tiles are in flight while one is multiplied.  Addresses are clamped
+// the tiles of the next stages are in flight while one is multiplied.  Addresses are clamped
 // into the operand (rows >= R read row R-1, k past the end reads the last
 // chunk); rows beyond R only feed discarded outputs and the k tail of the last
 // tile is zeroed in LDS before use.
@@ -102,16 +103,16 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 #define LDS_PTR(p) ((__attribute__((address_space(3))) void*)(p))
 
-// Issue this wave's share of the direct-to-LDS copies of one ROWS x BKV tile.
+// Issue copy i (of BLOCKS / NWAVES) of this wave's share of the
+// direct-to-LDS copies of one ROWS x BKV tile: one 1 KB block.
 template <int ROWS, bool KMAJOR, int BKV, int NWAVES>
-__device__ __forceinline__ void issue_tile(const bf16_t* base, int64_t ld, int64_t r0, int64_t k0,
-                                           int64_t R, int64_t K, char* lds, int wave, int lane) {
+__device__ __forceinline__ void issue_block(const bf16_t* base, int64_t ld, int64_t r0, int64_t k0,
+                                            int64_t R, int64_t K, char* lds, int wave, int lane, int i) {
   constexpr int BLOCKS = ROWS * BKV * 2 / 1024;  // 1 KB blocks per tile
-  constexpr int PER_WAVE = (BLOCKS + NWAVES - 1) / NWAVES;
-#pragma unroll
-  for (int i = 0; i < PER_WAVE; ++i) {
+  static_assert(BLOCKS % NWAVES == 0, "copies must split evenly over the waves");
+  constexpr int PER_WAVE = BLOCKS / NWAVES;
+  {
     const int blk = wave * PER_WAVE + i;
-    if (BLOCKS % NWAVES != 0 && blk >= BLOCKS) break;
     const bf16_t* src;
     if (KMAJOR) {
       constexpr int KCH = BKV / 8;           // 16-byte chunks per row
@@ -243,20 +244,26 @@ __device__ __forceinline__ void barrier_only() {
 // WGM x WGN waves per workgroup; each wave owns a (BM/WGM) x (BN/WGN) block of
 // 32x32 MFMA tiles.  More waves issue more direct-to-LDS copies in parallel
 // (the copy rate per CU grows with the number of issuing waves).
-// STAGES LDS stages of (BM + BN) x 32 bf16; OCC workgroups per CU.
+// STAGES LDS stages of the BM x BKV A tile and SBS (default: STAGES) of the
+// BN x BKV B tile; OCC workgroups per CU.  With one more A stage than B
+// stages, A's copies run one K step further ahead (the streamed activation
+// operand arrives from HBM/MALL while the weight operand hits L2).
 template <int BM, int BN, int WGM, int WGN, int STAGES, int OCC, bool AK, bool BKM, int EPI, bool SPLIT,
-          int BKV = 32>
+          int BKV = 32, int SBS = 0>
 __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KArgs P) {
   constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int A_BYTES = BM * BKV * 2, STAGE = (BM + BN) * BKV * 2;
-  constexpr int A_BLK = BM * BKV * 2 / 1024, B_BLK = BN * BKV * 2 / 1024;
+  constexpr int SA = STAGES, SB = SBS ? SBS : STAGES;
+  constexpr int LA = SA - 1, LB = SB - 1;  // copy lead of A and B, in K steps
+  static_assert(LB >= 1 && (LA == LB || LA == LB + 1), "A leads B by at most one step");
+  constexpr int A_BYTES = BM * BKV * 2, B_BYTES = BN * BKV * 2;
+  constexpr int A_BLK = A_BYTES / 1024, B_BLK = B_BYTES / 1024;
   // direct-to-LDS instructions per wave per K step (same count on every wave)
-  constexpr int LOADS = (A_BLK + NW - 1) / NW + (B_BLK + NW - 1) / NW;
+  constexpr int LOADS_A = (A_BLK + NW - 1) / NW, LOADS_B = (B_BLK + NW - 1) / NW;
   static_assert(A_BLK % NW == 0 && B_BLK % NW == 0, "copies must split evenly over the waves");
   constexpr int KS = BKV / 16;
-  __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[SA * A_BYTES + SB * B_BYTES];
 
   // ---- tile mapping.  The grid is one dimension of (batch or split) x
   // tiles, padded to a multiple of 8.  Workgroups are dealt round-robin over
@@ -310,58 +317,102 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
 #pragma unroll
   for (int x = 0; x < NA; ++x) a_off[x] = frag_lane_off<BM, AK, BKV>(wm * WM, x, lane);
 #pragma unroll
-  for (int x = 0; x < NB; ++x) b_off[x] = A_BYTES + frag_lane_off<BN, BKM, BKV>(wn * WN, x, lane);
+  for (int x = 0; x < NB; ++x) b_off[x] = frag_lane_off<BN, BKM, BKV>(wn * WN, x, lane);
   // LDS reads issued per sub-step
   constexpr int NREAD = TM * (AK ? 1 : 2) + TN * (BKM ? 1 : 2);
   const uint32_t lds0 = lds_addr(smem);
 
   const int nk = (int)((ke - kb + BKV - 1) / BKV);
   const int krem = (int)((ke - kb) - (int64_t)(nk - 1) * BKV);  // valid k in the last step
-  auto issue = [&](int t) {
-    char* st = smem + (t % STAGES) * STAGE;
-    const int64_t k0 = kb + (int64_t)t * BKV;
-    issue_tile<BM, AK, BKV, NW>(Ab, P.lda, m0, k0, P.M, ke, st, wave, lane);
-    issue_tile<BN, BKM, BKV, NW>(Bb, P.ldb, n0, k0, P.N, ke, st + A_BYTES, wave, lane);
+  char* const smem_b = smem + SA * A_BYTES;
+  // Copies of (virtual) step v: A tile v + LA and B tile v + LB, LOADS_A +
+  // LOADS_B one-block pieces per wave.  When A leads, B's pieces come first
+  // so that the wait for B(kt) leaves A(kt+1) in flight; when they lead
+  // equally, A's first (A(kt) older than B(kt)).
+  constexpr int NPIECE = LOADS_A + LOADS_B;
+  // With two or fewer stages of lead the copies are issued as early as
+  // possible (right after the first fragment reads); with three or more they
+  // are spread over the sub-steps (measured: each choice is 5-10 % faster
+  // where it is used).
+  constexpr bool SPREAD = LA >= 3;
+  auto issue_piece = [&](int v, int p) {
+    const bool is_b = LA > LB ? p < LOADS_B : p >= LOADS_A;
+    if (is_b) {
+      const int t = v + LB;
+      if (t >= 0 && t < nk)
+        issue_block<BN, BKM, BKV, NW>(Bb, P.ldb, n0, kb + (int64_t)t * BKV, P.N, ke, smem_b + (t % SB) * B_BYTES,
+                                      wave, lane, LA > LB ? p : p - LOADS_A);
+    } else {
+      const int t = v + LA;
+      if (t >= 0 && t < nk)
+        issue_block<BM, AK, BKV, NW>(Ab, P.lda, m0, kb + (int64_t)t * BKV, P.M, ke, smem + (t % SA) * A_BYTES,
+                                     wave, lane, LA > LB ? p - LOADS_B : p);
+    }
   };
 #pragma unroll
-  for (int t = 0; t < STAGES - 1; ++t)
-    if (t < nk) issue(t);
+  for (int v = -LA; v < 0; ++v)
+#pragma unroll
+    for (int p = 0; p < NPIECE; ++p) issue_piece(v, p);
 
   for (int kt = 0; kt < nk; ++kt) {
-    // tile kt has landed once at most the loads of the younger tiles are
-    // outstanding; the barrier publishes every wave's copies and frees the
-    // stage that was read in the previous step (every wave has waited for
-    // its reads of that stage before its last MFMAs)
-    const int younger = min(STAGES - 2, nk - 1 - kt);
-    static_for<0, STAGES - 1>([&](auto Y) {
-      constexpr int y = decltype(Y)::value;
-      static_assert(y * LOADS <= 63, "vmcnt field");
-      if (younger == y) WAIT_VMCNT(y * LOADS);
+    // A(kt) and B(kt) have landed once at most the loads issued after B(kt)
+    // are outstanding (loads complete in order): with d = the K steps left
+    // after this one (capped at LA), those are, for A leading, A(kt+1) and
+    // the copies of the LB-1 later steps, for equal leads the copies of the
+    // LB-1 later steps.  The barrier publishes every wave's copies and frees
+    // the stages read in the previous step (every wave has waited for its
+    // reads of them before its last MFMAs).
+    const int left = min(LA, nk - 1 - kt);
+    static_for<0, LA + 1>([&](auto D) {
+      constexpr int d = decltype(D)::value;
+      constexpr int y = [] {
+        int n = 0;
+        if (LA > LB) {
+          n += d >= 1 ? LOADS_A : 0;
+          for (int j = 1; j <= LB - 1; ++j) n += (j <= d ? LOADS_B : 0) + (j + 1 <= d ? LOADS_A : 0);
+        } else {
+          for (int j = 1; j <= LB - 1; ++j) n += j <= d ? LOADS_A + LOADS_B : 0;
+        }
+        return n;
+      }();
+      static_assert(y <= 63, "vmcnt field");
+      if (left == d) WAIT_VMCNT(y);
     });
     barrier_only();
-    char* st = smem + (kt % STAGES) * STAGE;
+    char* sta = smem + (kt % SA) * A_BYTES;
+    char* stb = smem_b + (kt % SB) * B_BYTES;
     if (kt == nk - 1 && krem < BKV) {
-      zero_tail<BM, AK, BKV>(st, krem);
-      zero_tail<BN, BKM, BKV>(st + A_BYTES, krem);
+      zero_tail<BM, AK, BKV>(sta, krem);
+      zero_tail<BN, BKM, BKV>(stb, krem);
       __syncthreads();
     }
-    const uint32_t sb = lds0 + (uint32_t)((kt % STAGES) * STAGE);
-    // the first sub-step's fragments are requested before the next stage's
-    // copies are issued (their address arithmetic hides the LDS latency);
-    // fragments of sub-step ks+1 are read while the MFMAs of ks run
-    u32x4 af[2][TM], bfr[2][TN];
-    read_frags<BM, AK, BKV, TM, 0>(sb, a_off, af[0]);
-    read_frags<BN, BKM, BKV, TN, 0>(sb, b_off, bfr[0]);
-    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1);
+    const uint32_t sa = lds0 + (uint32_t)((kt % SA) * A_BYTES);
+    const uint32_t sbb = lds0 + (uint32_t)(SA * A_BYTES + (kt % SB) * B_BYTES);
+    // the first PF sub-steps' fragments are requested before anything else
+    // (the copies' address arithmetic then hides the LDS latency);
+    // afterwards the fragments of sub-step ks+PF are read while the MFMAs of
+    // ks run.  LDS reads return in order, so waiting until at most the reads
+    // of the younger sub-steps are outstanding suffices.
+    constexpr int PF = 1;  // sub-steps of fragments in flight (2 measured slower)
+    constexpr int NBUF = PF + 1;
+    u32x4 af[NBUF][TM], bfr[NBUF][TN];
+    static_for<0, PF>([&](auto KSI) {
+      constexpr int ks = decltype(KSI)::value;
+      read_frags<BM, AK, BKV, TM, ks>(sa, a_off, af[ks]);
+      read_frags<BN, BKM, BKV, TN, ks>(sbb, b_off, bfr[ks]);
+    });
+    if constexpr (!SPREAD) {
+#pragma unroll
+      for (int p = 0; p < NPIECE; ++p) issue_piece(kt, p);
+    }
     static_for<0, KS>([&](auto KSI) {
-      constexpr int ks = decltype(KSI)::value, cb = ks & 1;
-      if constexpr (ks + 1 < KS) {
-        read_frags<BM, AK, BKV, TM, ks + 1>(sb, a_off, af[cb ^ 1]);
-        read_frags<BN, BKM, BKV, TN, ks + 1>(sb, b_off, bfr[cb ^ 1]);
-        lgkm_wait<NREAD>();
-      } else {
-        lgkm_wait<0>();
+      constexpr int ks = decltype(KSI)::value, cb = ks % NBUF;
+      if constexpr (ks + PF < KS) {
+        read_frags<BM, AK, BKV, TM, ks + PF>(sa, a_off, af[(ks + PF) % NBUF]);
+        read_frags<BN, BKM, BKV, TN, ks + PF>(sbb, b_off, bfr[(ks + PF) % NBUF]);
       }
+      constexpr int younger = (KS - 1 - ks < PF ? KS - 1 - ks : PF);
+      lgkm_wait<NREAD * younger>();
 #pragma unroll
       for (int i = 0; i < TM; ++i) after_wait(af[cb][i]);
 #pragma unroll
@@ -373,6 +424,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[cb][i]),
                                                               __builtin_bit_cast(bf16x8, bfr[cb][j]),
                                                               acc[i][j], 0, 0, 0);
+      // deep pipelines: this sub-step's share of the next stage's copies,
+      // whose address arithmetic runs while the MFMAs just issued execute
+      if constexpr (SPREAD) {
+#pragma unroll
+        for (int p = ks * NPIECE / KS; p < (ks + 1) * NPIECE / KS; ++p) issue_piece(kt, p);
+      }
     });
   }
 
@@ -469,7 +526,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI, int BKV = 32>
+template <int BM, int BN, int WGM, int WGN, int STG, int OCC, bool AK, bool BKM, int EPI, int BKV = 32,
+          int SBS = 0>
 hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   const int64_t n_log = (int64_t)P.tiles_m * P.tiles_n * (P.splits > 1 ? P.splits : batch);
   if (n_log >= (1ll << 31) - 8) return hipErrorInvalidValue;
@@ -477,7 +535,7 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
   constexpr int NT = 64 * WGM * WGN;
   if constexpr (EPI == EPI_F32 || EPI == EPI_UPDATE) {
     if (P.splits > 1) {
-      gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true, BKV><<<grid, NT, 0, s>>>(P);
+      gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true, BKV, SBS><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       const dim3 rgrid((unsigned)cdiv(P.N, 1024), (unsigned)P.M);
@@ -485,7 +543,7 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, false, BKV><<<grid, NT, 0, s>>>(P);
+  gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, false, BKV, SBS><<<grid, NT, 0, s>>>(P);
   return hipGetLastError();
 }
 
