@@ -577,12 +577,118 @@ __global__ void mean_kernel(const float* x, int64_t n, float* out) {
   if (threadIdx.x == 0) *out = s / (float)n;
 }
 
+// e^d for d <= 0 to about an ulp with the hardware base-2 exponential: the
+// argument d*log2(e) is split into an integer n and a remainder f in
+// [-1/2, 1/2] that carries the product's low bits (log2(e) as a two-float
+// sum), so exp2 sees an argument whose rounding error is ~2^-25 absolute.
+__device__ __forceinline__ float exp_acc(float d) {
+  const float L2E_HI = 1.44269502162933349609375f;       // float nearest log2(e)
+  const float L2E_LO = 1.925963033500011079e-08f;        // log2(e) - L2E_HI
+  const float n = __builtin_rintf(d * L2E_HI);
+  float f = fmaf(d, L2E_HI, -n);
+  f = fmaf(d, L2E_LO, f);
+  return __builtin_ldexpf(__builtin_amdgcn_exp2f(f), (int)n);
+}
+
+// Register-resident form for rows of at most CE_T x CE_CH 16-byte vectors
+// (V <= 53248; wider rows take ce_kernel): each of CE_T threads loads its vectors once (all loads in
+// flight together), so the row is read from HBM once; the exponentials are
+// cheap (exp_acc) and taken again for the gradient.  The maximum is exact;
+// the sum of e^(z - max) is accumulated in double precision in a fixed order
+// (per thread, then a shuffle tree, then the waves in order), so the
+// normaliser is within about an ulp of the exact one.  Deterministic.
+constexpr int CE_T = 512;
+template <int CE_CH>
+__global__ __launch_bounds__(CE_T) void ce_regs_kernel(const bf16_t* z, int64_t ld, const int32_t* tokens,
+                                                       int T, int V, int64_t n_rows, bf16_t* dz,
+                                                       float* loss_rows) {
+  constexpr int NW = CE_T / 64;
+  __shared__ float rmax[NW];
+  __shared__ double rsum[NW];
+  const int64_t row = blockIdx.x;
+  const int b = (int)(row / T), t = (int)(row % T);
+  int tgt = tokens[(int64_t)b * (T + 1) + t + 1];
+  const bool valid = tgt >= 0 && tgt < V;  // an invalid target adds no loss and no gradient
+  if (!valid) tgt = 0;
+  const u32x4* zr = reinterpret_cast<const u32x4*>(z + row * ld);
+  const int nv = (int)(ld / 8);
+  const float zt = bf2f(z[row * ld + tgt]);
+  u32x4 w[CE_CH];
+#pragma unroll
+  for (int c = 0; c < CE_CH; ++c) {
+    const int v = threadIdx.x + CE_T * c;
+    if (v < nv) w[c] = zr[v];
+  }
+  auto val = [&](int c, int e) {  // element e of this thread's vector c, -inf past V
+    const int j = 8 * (threadIdx.x + CE_T * c) + e;
+    const uint32_t u = w[c][e >> 1];
+    const float x = __builtin_bit_cast(float, (e & 1) ? (u & 0xffff0000u) : (u << 16));
+    return j < V ? x : -INFINITY;
+  };
+  float m = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < CE_CH; ++c)
+    if (threadIdx.x + CE_T * c < nv)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) m = fmaxf(m, val(c, e));
+  m = warp_max(m);
+  if ((threadIdx.x & 63) == 0) rmax[threadIdx.x >> 6] = m;
+  __syncthreads();
+  float M = rmax[0];
+#pragma unroll
+  for (int q = 1; q < NW; ++q) M = fmaxf(M, rmax[q]);
+  // e^(z - max), 0 past V; taken again (bitwise the same) for the gradient
+  auto prob = [&](int c, int e) {
+    const float x = val(c, e);
+    return x == -INFINITY ? 0.f : exp_acc(x - M);
+  };
+  double sum = 0.0;
+#pragma unroll
+  for (int c = 0; c < CE_CH; ++c)
+    if (threadIdx.x + CE_T * c < nv)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sum += (double)prob(c, e);
+  for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+  if ((threadIdx.x & 63) == 0) rsum[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  double S = 0.0;
+#pragma unroll
+  for (int q = 0; q < NW; ++q) S += rsum[q];
+  const float inv = (float)(1.0 / S);
+  const float scale = 1.0f / (float)n_rows;
+  u32x4* dr = reinterpret_cast<u32x4*>(dz + row * ld);
+#pragma unroll
+  for (int c = 0; c < CE_CH; ++c) {
+    const int v = threadIdx.x + CE_T * c;
+    if (v >= nv) continue;
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float g[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int j = 8 * v + 2 * k + h;
+        g[h] = valid ? (prob(c, 2 * k + h) * inv - (j == tgt ? 1.0f : 0.0f)) * scale : 0.f;
+      }
+      o[k] = pack_bf2(g[0], g[1]);
+    }
+    dr[v] = o;
+  }
+  if (threadIdx.x == 0) loss_rows[row] = valid ? (float)(log(S) + (double)M - (double)zt) : 0.0f;
+}
+
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B, int T,
                              int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
                              hipStream_t s) {
   if (ld % 8 || ld < V) return hipErrorInvalidValue;
   const int64_t rows = (int64_t)B * T;
-  ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+  const int64_t nv = ld / 8;
+  if (nv <= CE_T * 4)
+    ce_regs_kernel<4><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+  else if (nv <= CE_T * 13)  // GPT-2's 50304-column logits
+    ce_regs_kernel<13><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+  else
+    ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !loss_out) return e;
   mean_kernel<<<1, 1024, 0, s>>>(loss_rows, rows, loss_out);
