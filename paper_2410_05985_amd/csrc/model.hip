@@ -186,12 +186,28 @@ struct layup_ctx {
   float* dx[2] = {nullptr, nullptr};
   float* dh = nullptr;
   float* da = nullptr;
-  bf16_t *dy16 = nullptr, *df16 = nullptr, *do16 = nullptr, *dqkv16 = nullptr;
-  float *ln_part = nullptr, *cs_part = nullptr;
+  bf16_t* do16 = nullptr;
+  // The operands a linear layer's dW GEMM and bias sum read (dY), double-
+  // buffered by block parity: when the update stream differs from the
+  // compute stream, those dW GEMMs and sums run on the update stream,
+  // concurrently with the next layers' backward on the compute stream.
+  //   dyA: bf16 of the block's output gradient (MLP output projection)
+  //   dfb: GELU backward (MLP input projection)
+  //   dyB: bf16 of the gradient after the attention residual (attention proj)
+  //   dqb: dQ, dK, dV (qkv projection)
+  bf16_t *dyA[2] = {nullptr, nullptr}, *dfb[2] = {nullptr, nullptr};
+  bf16_t *dyB[2] = {nullptr, nullptr}, *dqb[2] = {nullptr, nullptr};
+  // ev_wr[k][p]: operand k of parity p written (compute stream);
+  // ev_rd[k][p]: its dW GEMM and bias sum done (update stream);
+  // ev_dx: a dX GEMM issued (fused schedule: dW runs after it)
+  hipEvent_t ev_wr[4][2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
+  float *ln_part = nullptr, *cs_part = nullptr, *cs_part_su = nullptr;
   int64_t cs_part_floats = 0;
   ColsumScratch cs() const { return ColsumScratch{cs_part, cs_part_floats}; }
-  float* splitk = nullptr;
-  size_t splitk_bytes = 0;
+  ColsumScratch cs_su() const { return ColsumScratch{cs_part_su, cs_part_floats}; }
+  float *splitk = nullptr, *splitk_su = nullptr;
+  size_t splitk_bytes = 0, splitk_su_bytes = 0;
+  bool dw_side() const { return su != sc; }
   float* dis_partial = nullptr;
   // MLP
   std::vector<float*> mlp_act;  // input copy not kept: act[0] = x pointer of the step
@@ -204,6 +220,7 @@ struct layup_ctx {
 namespace {
 
 constexpr size_t SPLITK_BYTES = 256u << 20;  // room for an 8-way split of an 8192 x 768 float32 output
+constexpr size_t SPLITK_SU_BYTES = 128u << 20;  // split-K of the dW GEMMs on the update stream
 
 size_t carve(layup_ctx* c, char* base) {
   Carver cv{base};
@@ -245,15 +262,21 @@ size_t carve(layup_ctx* c, char* base) {
     c->dx[1] = cv.take<float>(N * d);
     c->dh = cv.take<float>(N * d);
     c->da = cv.take<float>(N * d);
-    c->dy16 = cv.take<bf16_t>(N * d);
-    c->df16 = cv.take<bf16_t>(N * F);
+    for (int q = 0; q < 2; ++q) {
+      c->dyA[q] = cv.take<bf16_t>(N * d);
+      c->dfb[q] = cv.take<bf16_t>(N * F);
+      c->dyB[q] = cv.take<bf16_t>(N * d);
+      c->dqb[q] = cv.take<bf16_t>(N * 3 * d);
+    }
     c->do16 = cv.take<bf16_t>(N * d);
-    c->dqkv16 = cv.take<bf16_t>(N * 3 * d);
     c->ln_part = cv.take<float>(cdiv(N, 16) * 2 * d);
     c->cs_part_floats = cdiv(N, 128) * std::max<int64_t>(3 * d, F);
     c->cs_part = cv.take<float>(c->cs_part_floats);
+    c->cs_part_su = cv.take<float>(c->cs_part_floats);
     c->splitk = cv.take<float>(SPLITK_BYTES / 4);
     c->splitk_bytes = SPLITK_BYTES;
+    c->splitk_su = cv.take<float>(SPLITK_SU_BYTES / 4);
+    c->splitk_su_bytes = SPLITK_SU_BYTES;
   } else {
     const int n = g.n_mlp_layers;
     c->mlp_act.assign(n + 1, nullptr);
@@ -338,8 +361,9 @@ Gemm mk(bool ak, bool bk, int64_t M, int64_t N, int64_t K, const void* A, int64_
 // timed: one of a block's linear-layer backward GEMMs (dX or dW); with GEMM
 // timing on, HIP events on its stream bracket the launch (and its split-K sum)
 layup_status run_gemm(layup_ctx* c, Gemm g, hipStream_t s, const char* what, bool timed = false) {
-  g.splitk_ws = c->splitk;
-  g.splitk_ws_bytes = c->splitk_bytes;
+  const bool side = s != c->sc;  // the update stream has a split-K workspace of its own
+  g.splitk_ws = side ? c->splitk_su : c->splitk;
+  g.splitk_ws_bytes = side ? c->splitk_su_bytes : c->splitk_bytes;
   std::string m = gemm_check(g, false);
   if (!m.empty()) return fail(c, LAYUP_ERR_SHAPE, std::string(what) + ": " + m);
   timed = timed && c->gemm_timing;
@@ -448,16 +472,30 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                 dh = d / H, Vp = align64(g.vocab);
   const float scale = 1.0f / sqrtf((float)dh);
   Flat fl{c};
+  // dW GEMMs and bias sums go to the update stream when it is a different
+  // stream (sw); the events order them against the compute stream (s): an
+  // operand is read there only after s wrote it, and s overwrites it only
+  // after those reads (two blocks later, by parity)
+  const bool side = c->dw_side();
+  const hipStream_t sw = c->su;
+  auto rec = [&](hipEvent_t e, hipStream_t st) { return side ? hipEventRecord(e, st) : hipSuccess; };
+  auto wait = [&](hipStream_t st, hipEvent_t e) { return side ? hipStreamWaitEvent(st, e, 0) : hipSuccess; };
+  enum { OP_A = 0, OP_F = 1, OP_B = 2, OP_Q = 3 };
   if (u == g.n_layer + 1) {
     // output head (tied wte) and final LayerNorm
     Gemm dx = mk(true, false, N, d, Vp, c->logits, Vp, fl.w16("wte"), d, c->da, d, EPI_F32);
     TRY(run_gemm(c, dx, s, "head dX"));
+    // the head's dW stays on the compute stream: both head GEMMs fill the
+    // GPU, and running them concurrently was slower than one after the other
     Gemm dw = mk(false, false, Vp, d, N, c->logits, Vp, c->xf, d, fl.g("wte"), d, EPI_F32);
     TRY(run_gemm(c, dw, s, "head dW"));
     c->cur_dx = 0;
+    const int q = (g.n_layer - 1) & 1;  // the last block's output-gradient operand
+    HIPCHK(c, wait(s, c->ev_rd[OP_A][q]), "wait operand free");
     HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
-                                   c->dx[0], c->dy16, c->ln_part, c->cs(), fl.g("lnf.g"), fl.g("lnf.b"), N,
+                                   c->dx[0], c->dyA[q], c->ln_part, c->cs(), fl.g("lnf.g"), fl.g("lnf.b"), N,
                                    (int)d, s), "lnf backward");
+    HIPCHK(c, rec(c->ev_wr[OP_A][q], s), "record operand written");
     return LAYUP_OK;
   }
   if (u == 0) {
@@ -466,45 +504,56 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     return LAYUP_OK;
   }
   const int l = u - 1;
+  const int pq = l & 1;
   const BlockActs& A = c->acts[l];
   const std::string p = "h" + std::to_string(l) + ".";
   float* dxo = c->dx[c->cur_dx];
   float* dxi = c->dx[c->cur_dx ^ 1];
-  // Every linear layer: dW, db and dX.  In the fused schedule dX runs first
-  // (it reads the weight before its update) and the dW GEMM updates the
-  // weight in place.
+  bf16_t *dyA = c->dyA[pq], *df16 = c->dfb[pq], *dyB = c->dyB[pq], *dq16 = c->dqb[pq];
+  // Every linear layer: dX on the compute stream (the critical path), then
+  // dW and db.  In the fused schedule the dW GEMM updates the weight in
+  // place, so it waits for the layer's dX (which reads the weight first).
   const bool fz = c->fused_dw;
-  // MLP output projection
-  // c->dy16 holds bf16(dxo), written by the LayerNorm backward that produced dxo
-  Gemm dg = mk(true, false, N, F, d, c->dy16, d, fl.w16(p + "mproj.w"), F, c->df16, F, EPI_DGELU);
+  auto weight_grads = [&](int op, Gemm dw, const std::string& wname, const bf16_t* dy, int64_t cols,
+                          const char* bname, const char* what, const char* bwhat) -> layup_status {
+    HIPCHK(c, wait(sw, c->ev_wr[op][pq]), "wait operand written");
+    if (fz) {
+      HIPCHK(c, rec(c->ev_dx, s), "record dX issued");
+      HIPCHK(c, wait(sw, c->ev_dx), "wait dX");
+    }
+    TRY(run_gemm(c, dw_gemm(c, dw, wname), sw, what, true));
+    HIPCHK(c, launch_colsum_bf16(dy, N, cols, cols, side ? c->cs_su() : c->cs(), fl.g(p + bname), sw), bwhat);
+    HIPCHK(c, rec(c->ev_rd[op][pq], sw), "record operand read");
+    return LAYUP_OK;
+  };
+  // MLP output projection: dY = dyA (written by the LayerNorm backward that produced dxo)
+  Gemm dg = mk(true, false, N, F, d, dyA, d, fl.w16(p + "mproj.w"), F, df16, F, EPI_DGELU);
   dg.aux = A.f;
-  if (fz) TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
-  TRY(run_gemm(c, dw_gemm(c, mk(false, false, d, F, N, c->dy16, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
-                          p + "mproj.w"), s, "mproj dW", true));
-  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "mproj.b"), s), "mproj db");
-  if (!fz) TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
-  // MLP input projection
-  Gemm fcx = mk(true, false, N, d, F, c->df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
-  if (fz) TRY(run_gemm(c, fcx, s, "fc dX", true));
-  TRY(run_gemm(c, dw_gemm(c, mk(false, false, F, d, N, c->df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
-                          p + "fc.w"), s, "fc dW", true));
-  HIPCHK(c, launch_colsum_bf16(c->df16, N, F, F, c->cs(), fl.g(p + "fc.b"), s), "fc db");
-  if (!fz) TRY(run_gemm(c, fcx, s, "fc dX", true));
+  HIPCHK(c, wait(s, c->ev_rd[OP_F][pq]), "wait operand free");
+  TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
+  HIPCHK(c, rec(c->ev_wr[OP_F][pq], s), "record operand written");
+  TRY(weight_grads(OP_A, mk(false, false, d, F, N, dyA, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
+                   p + "mproj.w", dyA, d, "mproj.b", "mproj dW", "mproj db"));
+  // MLP input projection: dY = df16
+  Gemm fcx = mk(true, false, N, d, F, df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
+  TRY(run_gemm(c, fcx, s, "fc dX", true));
+  TRY(weight_grads(OP_F, mk(false, false, F, d, N, df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
+                   p + "fc.w", df16, F, "fc.b", "fc dW", "fc db"));
+  HIPCHK(c, wait(s, c->ev_rd[OP_B][pq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
-                                 c->dy16, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
+                                 dyB, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
-  // attention output projection
-  // c->dy16 now holds bf16(dh) from the LayerNorm backward above
-  Gemm prx = mk(true, false, N, d, d, c->dy16, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
-  if (fz) TRY(run_gemm(c, prx, s, "proj dX", true));
-  TRY(run_gemm(c, dw_gemm(c, mk(false, false, d, d, N, c->dy16, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32),
-                          p + "proj.w"), s, "proj dW", true));
-  HIPCHK(c, launch_colsum_bf16(c->dy16, N, d, d, c->cs(), fl.g(p + "proj.b"), s), "proj db");
-  if (!fz) TRY(run_gemm(c, prx, s, "proj dX", true));
+  HIPCHK(c, rec(c->ev_wr[OP_B][pq], s), "record operand written");
+  // attention output projection: dY = dyB = bf16(dh) from the LayerNorm backward above
+  Gemm prx = mk(true, false, N, d, d, dyB, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
+  TRY(run_gemm(c, prx, s, "proj dX", true));
+  TRY(weight_grads(OP_B, mk(false, false, d, d, N, dyB, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32),
+                   p + "proj.w", dyB, d, "proj.b", "proj dW", "proj db"));
+  HIPCHK(c, wait(s, c->ev_rd[OP_Q][pq]), "wait operand free");
   if (A.of) {
     // attention core, fused: dQ, dK, dV from recomputed scores (P and dS stay
     // in registers)
-    HIPCHK(c, launch_attention_bwd(A.qkv, A.lse, c->do16, A.of, c->att_D, c->dqkv16, (int)B, (int)H,
+    HIPCHK(c, launch_attention_bwd(A.qkv, A.lse, c->do16, A.of, c->att_D, dq16, (int)B, (int)H,
                                    (int)T, (int)dh, scale, s), "attention backward");
   } else {
     // attention core, batched over z = b*H + h
@@ -526,27 +575,30 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     TRY(run_gemm(c, batched(mk(true, true, T, T, dh, c->do16, d, A.qkv + 2 * d, 3 * d, c->S, T, EPI_F32),
                             T * d, dh, T * 3 * d, dh, H * TT, TT, CAUSAL_OUT_LOWER), s, "dP"));
     // dV_h = P^T dO_h
-    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, c->dqkv16 + 2 * d, 3 * d,
+    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, A.P, T, c->do16, d, dq16 + 2 * d, 3 * d,
                                EPI_BF16), H * TT, TT, T * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dV"));
     HIPCHK(c, launch_softmax_bwd(c->S, A.P, c->dS, B * H, (int)T, scale, s), "softmax backward");
     // dQ_h = dS K_h
-    TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, c->dqkv16, 3 * d,
+    TRY(run_gemm(c, batched(mk(true, false, T, dh, T, c->dS, T, A.qkv + d, 3 * d, dq16, 3 * d,
                                EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_LOWER), s, "dQ"));
     // dK_h = dS^T Q_h
-    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, c->dqkv16 + d, 3 * d,
+    TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, dq16 + d, 3 * d,
                                EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   }
-  // qkv projection
-  Gemm qx = mk(true, false, N, d, 3 * d, c->dqkv16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
-  if (fz) TRY(run_gemm(c, qx, s, "qkv dX", true));
-  TRY(run_gemm(c, dw_gemm(c, mk(false, false, 3 * d, d, N, c->dqkv16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d,
-                                EPI_F32), p + "qkv.w"), s, "qkv dW", true));
-  HIPCHK(c, launch_colsum_bf16(c->dqkv16, N, 3 * d, 3 * d, c->cs(), fl.g(p + "qkv.b"), s), "qkv db");
-  if (!fz) TRY(run_gemm(c, qx, s, "qkv dX", true));
+  HIPCHK(c, rec(c->ev_wr[OP_Q][pq], s), "record operand written");
+  // qkv projection: dY = dq16
+  Gemm qx = mk(true, false, N, d, 3 * d, dq16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
+  TRY(run_gemm(c, qx, s, "qkv dX", true));
+  TRY(weight_grads(OP_Q, mk(false, false, 3 * d, d, N, dq16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d, EPI_F32),
+                   p + "qkv.w", dq16, 3 * d, "qkv.b", "qkv dW", "qkv db"));
+  // LayerNorm 1; its bf16 dx is the next block's output-gradient operand
+  const int nq = pq ^ 1;
+  if (l > 0) HIPCHK(c, wait(s, c->ev_rd[OP_A][nq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
-                                 l > 0 ? c->dy16 : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
+                                 l > 0 ? c->dyA[nq] : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
                                  fl.g(p + "ln1.b"), N, (int)d,
                                  s), "ln1 backward");
+  if (l > 0) HIPCHK(c, rec(c->ev_wr[OP_A][nq], s), "record operand written");
   c->cur_dx ^= 1;
   return LAYUP_OK;
 }
@@ -797,6 +849,16 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
     layup_destroy(c);
     return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
   }
+  // ordering events between the compute stream and the update stream's dW work
+  bool ev_ok = hipEventCreateWithFlags(&c->ev_dx, hipEventDisableTiming) == hipSuccess;
+  for (int k = 0; k < 4; ++k)
+    for (int q = 0; q < 2; ++q)
+      ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_wr[k][q], hipEventDisableTiming) == hipSuccess &&
+              hipEventCreateWithFlags(&c->ev_rd[k][q], hipEventDisableTiming) == hipSuccess;
+  if (!ev_ok) {
+    layup_destroy(c);
+    return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
+  }
   *out = c;
   return LAYUP_OK;
 }
@@ -811,6 +873,13 @@ void layup_destroy(layup_ctx* ctx) {
   if (ctx->ev_start) hipEventDestroy(ctx->ev_start);
   if (ctx->ev_fwd_end) hipEventDestroy(ctx->ev_fwd_end);
   if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
+  for (auto& row : ctx->ev_wr)
+    for (auto e : row)
+      if (e) hipEventDestroy(e);
+  for (auto& row : ctx->ev_rd)
+    for (auto e : row)
+      if (e) hipEventDestroy(e);
+  if (ctx->ev_dx) hipEventDestroy(ctx->ev_dx);
   delete ctx;
 }
 
@@ -859,6 +928,12 @@ layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit) {
   layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_backward(ctx, unit) : mlp_backward(ctx, unit);
   if (st != LAYUP_OK) return st;
   HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->sc), "record unit event");
+  if (ctx->dw_side()) {
+    // the unit's gradients are complete once both streams' parts are: the
+    // event is re-recorded on the update stream behind the compute stream's
+    HIPCHK(ctx, hipStreamWaitEvent(ctx->su, ctx->ev_unit[unit], 0), "wait unit event");
+    HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->su), "record unit event");
+  }
   ctx->backward_done[unit] = 1;
   ctx->next_backward--;
   if (ctx->next_backward < 0) ctx->forward_done = false;
