@@ -25,7 +25,7 @@ def compare(gpu, ref, rtol, name=""):
     return worst, normwise
 
 
-def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0):
+def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0, exact=None):
     """Rule for results that went through a chain of bfloat16 storage points
     on both sides (a whole forward + backward).  Where a float32 value and its
     float64 counterpart straddle a bf16 rounding boundary the two sides store
@@ -33,7 +33,13 @@ def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0):
     so after a few stages the discrepancy settles near one bf16 ulp (2**-8
     relative) in norm, with rare larger elements.  Bar: normwise error <= rtol,
     at most ``frac`` of the elements outside rtol * (|ref| + rms), none
-    outside cap * rtol * (|ref| + rms)."""
+    outside cap * rtol * (|ref| + rms).
+
+    ``exact``, when given, is the oracle's result with no storage rounding
+    (exact arithmetic).  How often the bf16-storage oracle itself lands
+    beyond rtol from it measures the spread that bf16 storage alone causes;
+    the GPU, a second bf16-storage pipeline, may have as many elements
+    beyond rtol from the oracle as the oracle has from exact arithmetic."""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert gpu.shape == ref.shape, (name, gpu.shape, ref.shape)
@@ -47,6 +53,11 @@ def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0):
     n_out = int(np.sum(ratio > rtol))
     worst = float(ratio.max())
     assert normwise <= rtol, f"{name}: normwise {normwise:.3e} > {rtol}"
-    assert n_out <= max(frac * ratio.size, 0), f"{name}: {n_out}/{ratio.size} elements beyond {rtol}"
+    allowed = frac * ratio.size
+    if exact is not None:
+        exact = np.asarray(exact, np.float64)
+        assert exact.shape == ref.shape, (name, exact.shape, ref.shape)
+        allowed = max(allowed, int(np.sum(np.abs(exact - ref) / np.maximum(scale, 1e-300) > rtol)))
+    assert n_out <= allowed, f"{name}: {n_out}/{ratio.size} elements beyond {rtol} (allowed {allowed:.0f})"
     assert worst <= cap * rtol, f"{name}: worst element {worst:.3e} > {cap * rtol}"
     return worst, normwise
