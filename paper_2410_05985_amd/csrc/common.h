@@ -27,6 +27,19 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// e^d to about an ulp with the hardware base-2 exponential (|d| < 87): the
+// argument d*log2(e) is split into an integer n and a remainder f in
+// [-1/2, 1/2] that carries the product's low bits (log2(e) as a two-float
+// sum), so exp2 sees an argument whose rounding error is ~2^-25 absolute.
+__device__ __forceinline__ float exp_acc(float d) {
+  const float L2E_HI = 1.44269502162933349609375f;       // float nearest log2(e)
+  const float L2E_LO = 1.925963033500011079e-08f;        // log2(e) - L2E_HI
+  const float n = __builtin_rintf(d * L2E_HI);
+  float f = fmaf(d, L2E_HI, -n);
+  f = fmaf(d, L2E_LO, f);
+  return __builtin_ldexpf(__builtin_amdgcn_exp2f(f), (int)n);
+}
+
 __device__ __forceinline__ float warp_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;

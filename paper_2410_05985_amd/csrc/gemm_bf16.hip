@@ -46,17 +46,28 @@ struct KArgs {
   UpdArgs upd;             // EPI_UPDATE
 };
 
-__device__ __forceinline__ float gelu_tanh_f(float x) {
+// GELU, tanh form: 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(u)) = sigmoid(2u), it is x s with s = 1 / (1 + e),
+// e = e^(-2u): one accurate exponential and a reciprocal instead of tanh.
+// 1 - s = e s keeps its relative accuracy where s is close to 1.
+__device__ __forceinline__ float gelu_sig(float x, float& e) {
   const float c = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = c * fmaf(0.044715f * x, x * x, x);
-  return 0.5f * x * (1.0f + tanhf(u));
+  const float u = c * fmaf(0.044715f * x, x * x, x);
+  e = exp_acc(fminf(-2.0f * u, 80.0f));
+  return __builtin_amdgcn_rcpf(1.0f + e);
 }
 
+__device__ __forceinline__ float gelu_tanh_f(float x) {
+  float e;
+  return x * gelu_sig(x, e);
+}
+
+// d/dx GELU = s + x s (1 - s) 2 sqrt(2/pi) (1 + 3 0.044715 x^2)
 __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
-  const float c = 0.7978845608028654f;
-  float u = c * fmaf(0.044715f * x, x * x, x);
-  float t = tanhf(u);
-  return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * c * fmaf(3.0f * 0.044715f, x * x, 1.0f);
+  float e;
+  const float s = gelu_sig(x, e);
+  const float c2 = 2.0f * 0.7978845608028654f;
+  return fmaf(x * s * (e * s), c2 * fmaf(3.0f * 0.044715f, x * x, 1.0f), s);
 }
 
 // ------------------------------------------------------------ pipeline

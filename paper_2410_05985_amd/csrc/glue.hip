@@ -577,19 +577,6 @@ __global__ void mean_kernel(const float* x, int64_t n, float* out) {
   if (threadIdx.x == 0) *out = s / (float)n;
 }
 
-// e^d for d <= 0 to about an ulp with the hardware base-2 exponential: the
-// argument d*log2(e) is split into an integer n and a remainder f in
-// [-1/2, 1/2] that carries the product's low bits (log2(e) as a two-float
-// sum), so exp2 sees an argument whose rounding error is ~2^-25 absolute.
-__device__ __forceinline__ float exp_acc(float d) {
-  const float L2E_HI = 1.44269502162933349609375f;       // float nearest log2(e)
-  const float L2E_LO = 1.925963033500011079e-08f;        // log2(e) - L2E_HI
-  const float n = __builtin_rintf(d * L2E_HI);
-  float f = fmaf(d, L2E_HI, -n);
-  f = fmaf(d, L2E_LO, f);
-  return __builtin_ldexpf(__builtin_amdgcn_exp2f(f), (int)n);
-}
-
 // Register-resident form for rows of at most CE_T x CE_CH 16-byte vectors
 // (V <= 53248; wider rows take ce_kernel): each of CE_T threads loads its vectors once (all loads in
 // flight together), so the row is read from HBM once; the exponentials are
