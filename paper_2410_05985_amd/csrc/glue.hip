@@ -167,77 +167,166 @@ hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, 
 }
 
 // LayerNorm backward.  dx = dres + r*(dxh - mean(dxh) - xh*mean(dxh*xh)) with
-// xh = (x-mean)*r and dxh = dy*g.  dg and db (column sums of dy*xh and dy)
-// are accumulated per block over LN_ROWS rows in fixed order into partial
-// rows, summed later by a column-sum kernel.
-constexpr int LN_ROWS = 16;
-constexpr int LN_MAXV = 8;  // float4 groups per lane: d <= 2048
+// xh = (x-mean)*r and dxh = dy*g.  A block of LN_WAVES waves takes LN_ROWS
+// rows; wave w takes rows w, w + LN_WAVES, ... and loads its next row while it
+// works on the current one, every operand of a row held in registers (NVL
+// float4 groups per lane, d <= 256*NVL; wider rows are read twice, and the
+// next-row prefetch is used while two rows fit in registers).  dg and db (column sums of dy*xh and
+// dy) are summed per wave in row order, then over the waves in wave order,
+// into one partial row per block; ln_partial_sum_kernel adds the partial rows
+// in block order.
+constexpr int LN_WAVES = 8;
+constexpr int LN_ROWS = 32;
 
-__global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, const float* x,
-                                                            const float* mean, const float* rstd,
-                                                            const float* g, const float* dres,
-                                                            float* dx, bf16_t* dx16, float* part,
-                                                            int64_t rows, int d) {
-  extern __shared__ f32x4 ln_red[];  // [2][4][nv]
+struct LnRow {
+  float mu, r;
+};
+
+template <int NVL>
+__device__ __forceinline__ void ln_load_row(const float* dy, const float* x, const float* dres,
+                                            const float* mean, const float* rstd, int64_t row,
+                                            int d, int lane, f32x4 (&a)[NVL], f32x4 (&xv)[NVL],
+                                            f32x4 (&o)[NVL], LnRow& st) {
+  const int nv = d / 4;
+  st.mu = mean[row];
+  st.r = rstd[row];
+#pragma unroll
+  for (int j = 0; j < NVL; ++j) {
+    const int i = lane + 64 * j;
+    const f32x4 z{0.f, 0.f, 0.f, 0.f};
+    a[j] = i < nv ? reinterpret_cast<const f32x4*>(dy + row * d)[i] : z;
+    xv[j] = i < nv ? reinterpret_cast<const f32x4*>(x + row * d)[i] : z;
+    o[j] = (dres && i < nv) ? reinterpret_cast<const f32x4*>(dres + row * d)[i] : z;
+  }
+}
+
+template <int NVL>
+__global__ __launch_bounds__(64 * LN_WAVES) void layernorm_bwd_kernel(
+    const float* dy, const float* x, const float* mean, const float* rstd, const float* g,
+    const float* dres, float* dx, bf16_t* dx16, float* part, int64_t rows, int d) {
+  extern __shared__ f32x4 ln_red[];  // [2][LN_WAVES][nv]
+  // HOLD: the row stays in registers between the two passes (else it is read
+  // again, from cache); PF: the next row is loaded during the current one.
+  constexpr bool HOLD = NVL <= 4, PF = NVL <= 3;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int nv = d / 4;
-  f32x4* red_g = ln_red;
-  f32x4* red_b = ln_red + 4 * nv;
-  f32x4 ag[LN_MAXV], ab[LN_MAXV];
+  const float inv_d = 1.0f / (float)d;
+  const f32x4 z{0.f, 0.f, 0.f, 0.f};
+  f32x4 gg[NVL], ag[NVL], ab[NVL];
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j) ag[j] = ab[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int64_t r0 = (int64_t)blockIdx.x * LN_ROWS;
-  for (int rr = w; rr < LN_ROWS; rr += 4) {
-    const int64_t row = r0 + rr;
+  for (int j = 0; j < NVL; ++j) {
+    const int i = lane + 64 * j;
+    gg[j] = i < nv ? reinterpret_cast<const f32x4*>(g)[i] : z;
+    ag[j] = ab[j] = z;
+  }
+  const int64_t r0 = (int64_t)blockIdx.x * LN_ROWS + w;
+  f32x4 a[HOLD ? NVL : 1], xv[HOLD ? NVL : 1], o[HOLD ? NVL : 1];
+  LnRow st{0.f, 0.f};
+  if constexpr (PF) {
+    if (r0 < rows) ln_load_row<NVL>(dy, x, dres, mean, rstd, r0, d, lane, a, xv, o, st);
+  }
+#pragma unroll
+  for (int k = 0; k < LN_ROWS / LN_WAVES; ++k) {
+    const int64_t row = r0 + (int64_t)k * LN_WAVES;
     if (row >= rows) break;
-    const float mu = mean[row], r = rstd[row];
     const f32x4* dyr = reinterpret_cast<const f32x4*>(dy + row * d);
     const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * d);
     float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-    for (int j = 0; j < LN_MAXV; ++j) {
-      int i = lane + 64 * j;
-      if (i >= nv) break;
-      f32x4 a = dyr[i], xv = xr[i], gg = reinterpret_cast<const f32x4*>(g)[i];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float xh = (xv[e] - mu) * r;
-        float dxh = a[e] * gg[e];
-        s1 += dxh;
-        s2 = fmaf(dxh, xh, s2);
-        ag[j][e] = fmaf(a[e], xh, ag[j][e]);
-        ab[j][e] += a[e];
+    if constexpr (HOLD) {
+      if constexpr (!PF) ln_load_row<NVL>(dy, x, dres, mean, rstd, row, d, lane, a, xv, o, st);
+      f32x4 a1[PF ? NVL : 1], x1[PF ? NVL : 1], o1[PF ? NVL : 1];
+      LnRow st1{0.f, 0.f};
+      const bool more = PF && k + 1 < LN_ROWS / LN_WAVES && row + LN_WAVES < rows;
+      if constexpr (PF) {
+        if (more) ln_load_row<NVL>(dy, x, dres, mean, rstd, row + LN_WAVES, d, lane, a1, x1, o1, st1);
       }
-    }
-    s1 = warp_sum(s1) / d;
-    s2 = warp_sum(s2) / d;
 #pragma unroll
-    for (int j = 0; j < LN_MAXV; ++j) {
-      int i = lane + 64 * j;
-      if (i >= nv) break;
-      f32x4 a = dyr[i], xv = xr[i], gg = reinterpret_cast<const f32x4*>(g)[i];
-      f32x4 o = dres ? reinterpret_cast<const f32x4*>(dres + row * d)[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < NVL; ++j) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        float xh = (xv[e] - mu) * r;
-        o[e] += r * (a[e] * gg[e] - s1 - xh * s2);
+        for (int e = 0; e < 4; ++e) {
+          const float xh = (xv[j][e] - st.mu) * st.r;
+          const float dxh = a[j][e] * gg[j][e];
+          s1 += dxh;
+          s2 = fmaf(dxh, xh, s2);
+          ag[j][e] = fmaf(a[j][e], xh, ag[j][e]);
+          ab[j][e] += a[j][e];
+        }
       }
-      reinterpret_cast<f32x4*>(dx + row * d)[i] = o;
-      if (dx16) reinterpret_cast<u32x2*>(dx16 + row * d)[i] = u32x2{pack_bf2(o[0], o[1]), pack_bf2(o[2], o[3])};
+      s1 = warp_sum(s1) * inv_d;
+      s2 = warp_sum(s2) * inv_d;
+#pragma unroll
+      for (int j = 0; j < NVL; ++j) {
+        const int i = lane + 64 * j;
+        if (i >= nv) break;
+        f32x4 v = o[j];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float xh = (xv[j][e] - st.mu) * st.r;
+          v[e] += st.r * (a[j][e] * gg[j][e] - s1 - xh * s2);
+        }
+        reinterpret_cast<f32x4*>(dx + row * d)[i] = v;
+        if (dx16) reinterpret_cast<u32x2*>(dx16 + row * d)[i] = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+      }
+      if constexpr (PF) {
+        if (more) {
+#pragma unroll
+          for (int j = 0; j < NVL; ++j) {
+            a[j] = a1[j];
+            xv[j] = x1[j];
+            o[j] = o1[j];
+          }
+          st = st1;
+        }
+      }
+    } else {
+      st.mu = mean[row];
+      st.r = rstd[row];
+#pragma unroll
+      for (int j = 0; j < NVL; ++j) {
+        const int i = lane + 64 * j;
+        const f32x4 av = i < nv ? dyr[i] : z, xx = i < nv ? xr[i] : z;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float xh = (xx[e] - st.mu) * st.r;
+          const float dxh = av[e] * gg[j][e];
+          s1 += dxh;
+          s2 = fmaf(dxh, xh, s2);
+          ag[j][e] = fmaf(av[e], xh, ag[j][e]);
+          ab[j][e] += av[e];
+        }
+      }
+      s1 = warp_sum(s1) * inv_d;
+      s2 = warp_sum(s2) * inv_d;
+#pragma unroll
+      for (int j = 0; j < NVL; ++j) {
+        const int i = lane + 64 * j;
+        if (i >= nv) break;
+        const f32x4 av = dyr[i], xx = xr[i];
+        f32x4 v = dres ? reinterpret_cast<const f32x4*>(dres + row * d)[i] : z;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float xh = (xx[e] - st.mu) * st.r;
+          v[e] += st.r * (av[e] * gg[j][e] - s1 - xh * s2);
+        }
+        reinterpret_cast<f32x4*>(dx + row * d)[i] = v;
+        if (dx16) reinterpret_cast<u32x2*>(dx16 + row * d)[i] = u32x2{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3])};
+      }
     }
   }
+  f32x4* red_g = ln_red;
+  f32x4* red_b = ln_red + LN_WAVES * nv;
 #pragma unroll
-  for (int j = 0; j < LN_MAXV; ++j) {
-    int i = lane + 64 * j;
+  for (int j = 0; j < NVL; ++j) {
+    const int i = lane + 64 * j;
     if (i < nv) {
       red_g[w * nv + i] = ag[j];
       red_b[w * nv + i] = ab[j];
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nv; i += 256) {
+  for (int i = threadIdx.x; i < nv; i += 64 * LN_WAVES) {
     f32x4 sg = red_g[i], sb = red_b[i];
-    for (int k = 1; k < 4; ++k) {
+    for (int k = 1; k < LN_WAVES; ++k) {
       sg += red_g[k * nv + i];
       sb += red_b[k * nv + i];
     }
@@ -247,22 +336,58 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(const float* dy, con
   }
 }
 
-template <typename T>
-hipError_t colsum2(const T* x, int64_t rows, int64_t cols, int64_t ld, const ColsumScratch& cs,
-                   float* out, float* out2, int64_t split, hipStream_t s);
+// dg | db = the nb partial rows [nb][2d] added in row order.  A block covers
+// 64 columns (16 float4 groups) with 16 row lanes: lane l adds rows l, l+16,
+// ... in order, then the 16 lane sums are added in lane order.
+__global__ __launch_bounds__(256) void ln_partial_sum_kernel(const float* part, int64_t nb, int d,
+                                                             float* dg, float* db) {
+  __shared__ f32x4 red[16][16];
+  const int cg = threadIdx.x & 15, rl = threadIdx.x >> 4;
+  const int64_t cols = 2 * (int64_t)d;
+  const int64_t c = ((int64_t)blockIdx.x * 16 + cg) * 4;
+  f32x4 s{0.f, 0.f, 0.f, 0.f};
+  if (c < cols) {
+#pragma unroll 4
+    for (int64_t r = rl; r < nb; r += 16) s += *reinterpret_cast<const f32x4*>(part + r * cols + c);
+  }
+  red[rl][cg] = s;
+  __syncthreads();
+  if (rl == 0 && c < cols) {
+    f32x4 t = red[0][cg];
+    for (int l = 1; l < 16; ++l) t += red[l][cg];
+    float* out = c < d ? dg + c : db + (c - d);
+    *reinterpret_cast<f32x4*>(out) = t;
+  }
+}
+
+template <int NVL>
+static hipError_t ln_bwd_launch(const float* dy, const float* x, const float* mean, const float* rstd,
+                                const float* g, const float* dres, float* dx, bf16_t* dx16, float* part,
+                                int64_t rows, int d, unsigned nb, hipStream_t s) {
+  const size_t lds = (size_t)2 * LN_WAVES * (d / 4) * sizeof(f32x4);
+  layernorm_bwd_kernel<NVL><<<nb, 64 * LN_WAVES, lds, s>>>(dy, x, mean, rstd, g, dres, dx, dx16, part,
+                                                           rows, d);
+  return hipGetLastError();
+}
+
+int64_t layernorm_bwd_partial_floats(int64_t rows, int d) { return cdiv(rows, LN_ROWS) * 2 * (int64_t)d; }
 
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres, float* dx,
-                                bf16_t* dx16, float* part, const ColsumScratch& cs, float* dg,
-                                float* db, int64_t rows, int d, hipStream_t s) {
-  if (d / 4 > LN_MAXV * 64) return hipErrorInvalidValue;
+                                bf16_t* dx16, float* part, float* dg, float* db, int64_t rows, int d,
+                                hipStream_t s) {
+  if (d % 4 != 0 || d > 256 * 8 || rows <= 0) return hipErrorInvalidValue;
   const unsigned nb = (unsigned)cdiv(rows, LN_ROWS);
-  const size_t lds = (size_t)2 * 4 * (d / 4) * sizeof(f32x4);
-  layernorm_bwd_kernel<<<nb, 256, lds, s>>>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d);
-  hipError_t e = hipGetLastError();
+  const int nvl = (int)cdiv(d / 4, 64);
+  hipError_t e;
+  if (nvl <= 1) e = ln_bwd_launch<1>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
+  else if (nvl == 2) e = ln_bwd_launch<2>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
+  else if (nvl == 3) e = ln_bwd_launch<3>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
+  else if (nvl == 4) e = ln_bwd_launch<4>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
+  else e = ln_bwd_launch<8>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
   if (e != hipSuccess) return e;
-  // dg and db: one column sum over the [nb][2d] partial rows
-  return colsum2<float>(part, nb, 2 * d, 2 * d, cs, dg, db, d, s);
+  ln_partial_sum_kernel<<<(unsigned)cdiv(2 * (int64_t)d, 64), 256, 0, s>>>(part, nb, d, dg, db);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------ column sums

@@ -167,12 +167,14 @@ struct ColsumScratch {
   int64_t partial_floats;
 };
 // LayerNorm backward: dx (float32) and optionally its bfloat16 copy dx16;
-// per-16-row partial sums of dg and db go to part (ceil(rows/16) x 2d floats)
-// and are reduced into dg, db.
+// per-block partial sums of dg and db go to part
+// (layernorm_bwd_partial_floats(rows, d) floats) and are added into dg, db
+// in a fixed order.  d a multiple of 4, at most 2048.
+int64_t layernorm_bwd_partial_floats(int64_t rows, int d);
 hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* mean,
                                 const float* rstd, const float* g, const float* dres,
-                                float* dx, bf16_t* dx16, float* part, const ColsumScratch& cs,
-                                float* dg, float* db, int64_t rows, int d, hipStream_t s);
+                                float* dx, bf16_t* dx16, float* part, float* dg, float* db,
+                                int64_t rows, int d, hipStream_t s);
 hipError_t launch_softmax_fwd(const float* S, bf16_t* P, int64_t n_mat, int T, float scale,
                               hipStream_t s);
 hipError_t launch_softmax_bwd(const float* dP, const bf16_t* P, bf16_t* dS, int64_t n_mat, int T,

@@ -269,7 +269,7 @@ size_t carve(layup_ctx* c, char* base) {
       c->dqb[q] = cv.take<bf16_t>(N * 3 * d);
     }
     c->do16 = cv.take<bf16_t>(N * d);
-    c->ln_part = cv.take<float>(cdiv(N, 16) * 2 * d);
+    c->ln_part = cv.take<float>(layernorm_bwd_partial_floats(N, (int)d));
     c->cs_part_floats = cdiv(N, 128) * std::max<int64_t>(3 * d, F);
     c->cs_part = cv.take<float>(c->cs_part_floats);
     c->cs_part_su = cv.take<float>(c->cs_part_floats);
@@ -493,7 +493,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     const int q = (g.n_layer - 1) & 1;  // the last block's output-gradient operand
     HIPCHK(c, wait(s, c->ev_rd[OP_A][q]), "wait operand free");
     HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
-                                   c->dx[0], c->dyA[q], c->ln_part, c->cs(), fl.g("lnf.g"), fl.g("lnf.b"), N,
+                                   c->dx[0], c->dyA[q], c->ln_part, fl.g("lnf.g"), fl.g("lnf.b"), N,
                                    (int)d, s), "lnf backward");
     HIPCHK(c, rec(c->ev_wr[OP_A][q], s), "record operand written");
     return LAYUP_OK;
@@ -541,7 +541,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                    p + "fc.w", df16, F, "fc.b", "fc dW", "fc db"));
   HIPCHK(c, wait(s, c->ev_rd[OP_B][pq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
-                                 dyB, c->ln_part, c->cs(), fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
+                                 dyB, c->ln_part, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
   HIPCHK(c, rec(c->ev_wr[OP_B][pq], s), "record operand written");
   // attention output projection: dY = dyB = bf16(dh) from the LayerNorm backward above
@@ -595,7 +595,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   const int nq = pq ^ 1;
   if (l > 0) HIPCHK(c, wait(s, c->ev_rd[OP_A][nq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.x, A.mean1, A.rstd1, fl.p(p + "ln1.g"), c->dh, dxi,
-                                 l > 0 ? c->dyA[nq] : nullptr, c->ln_part, c->cs(), fl.g(p + "ln1.g"),
+                                 l > 0 ? c->dyA[nq] : nullptr, c->ln_part, fl.g(p + "ln1.g"),
                                  fl.g(p + "ln1.b"), N, (int)d,
                                  s), "ln1 backward");
   if (l > 0) HIPCHK(c, rec(c->ev_wr[OP_A][nq], s), "record operand written");

@@ -105,6 +105,12 @@ GPT_TEST_LONG = GPTConfig(n_layer=1, d_model=128, n_head=2, d_ff=256, seq=512, b
                           vocab=400, name="gpt-test-long")
 GPT_TEST_DH48 = GPTConfig(n_layer=1, d_model=96, n_head=2, d_ff=256, seq=64, batch=2,
                           vocab=200, name="gpt-test-dh48")
+# Wide rows: 832 and 1088 features (208 and 272 float4 groups, ragged over
+# 64 lanes), the LayerNorm paths for rows wider than 768 features.
+GPT_TEST_W832 = GPTConfig(n_layer=1, d_model=832, n_head=13, d_ff=256, seq=64, batch=2,
+                          vocab=250, name="gpt-test-w832")
+GPT_TEST_W1088 = GPTConfig(n_layer=1, d_model=1088, n_head=17, d_ff=256, seq=64, batch=2,
+                           vocab=250, name="gpt-test-w1088")
 
 RESNET50_UPDATE = dict(lr=0.1, momentum=0.9, weight_decay=5e-5, alpha=0.5)
 

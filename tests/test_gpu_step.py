@@ -159,7 +159,8 @@ def test_gpt_forward_activations(cfg):
     m.close()
 
 
-@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48],
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48,
+                                 S.GPT_TEST_W832, S.GPT_TEST_W1088],
                          ids=lambda c: c.name)
 def test_gpt_step_parity(cfg):
     """One layer-wise step, chained: every gradient at rel 2e-2 (bf16 GEMM
@@ -176,19 +177,24 @@ def test_gpt_step_parity(cfg):
     om = {k: np.zeros_like(v) for k, v in op.items()}
     ov = {k: np.zeros_like(v) for k, v in op.items()}
     opeer = {k: v.astype(np.float64) for k, v in peers[0].items()}
+    # the same step in exact arithmetic, on copies: the spread bf16 storage
+    # alone causes in the gradients and moments
+    xp, xm, xv = ({k: a.copy() for k, a in d.items()} for d in (op, om, ov))
+    _, xgrads, _, _ = O.gpt_step(xp, xm, xv, opeer, tokens, cfg.n_head, ohp, cfg.alpha, rnd=O.ident)
     oloss, ograds, otrace, odis = O.gpt_step(op, om, ov, opeer, tokens, cfg.n_head, ohp, cfg.alpha)
     m.synchronize()
     assert abs(loss.item() - oloss) <= 2e-3 * abs(oloss)
     g = m.read("grads")
     for k, ref in ograds.items():
-        compare_chained(g[k], ref.reshape(g[k].shape), 2e-2, f"grad {k}")
+        compare_chained(g[k], ref.reshape(g[k].shape), 2e-2, f"grad {k}",
+                        exact=xgrads[k].reshape(g[k].shape))
     got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
     for k in op:
         shp = got_p[k].shape
         check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
                            f"param {k}")
-        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}")
-        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}")
+        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}", exact=xm[k].reshape(shp))
+        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}", exact=xv[k].reshape(shp))
     n_units = cfg.n_layer + 2
     assert otrace == list(range(n_units - 1, -1, -1))
     assert m.read_trace() == [(0, u) for u in otrace]
@@ -336,6 +342,8 @@ def test_fused_dw_schedule_matches_oracle(cfg):
     om = {k: np.zeros_like(v) for k, v in op.items()}
     ov = {k: np.zeros_like(v) for k, v in op.items()}
     opeer = {k: v.astype(np.float64) for k, v in peers[0].items()}
+    xp, xm, xv = ({k: a.copy() for k, a in d.items()} for d in (op, om, ov))
+    O.gpt_step(xp, xm, xv, opeer, tokens, cfg.n_head, ohp, cfg.alpha, rnd=O.ident)
     oloss, ograds, otrace, _ = O.gpt_step(op, om, ov, opeer, tokens, cfg.n_head, ohp, cfg.alpha)
     m.synchronize()
     assert abs(loss.item() - oloss) <= 2e-3 * abs(oloss)
@@ -344,8 +352,8 @@ def test_fused_dw_schedule_matches_oracle(cfg):
         shp = got_p[k].shape
         check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
                            f"param {k}")
-        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}")
-        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}")
+        compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}", exact=xm[k].reshape(shp))
+        compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}", exact=xv[k].reshape(shp))
     assert m.read_trace() == [(0, u) for u in otrace]
     p16 = (m.params_bf16.to(torch.int32) << 16).view(torch.float32).cpu().numpy()
     assert np.array_equal(p16, O.bf16(m.params.cpu().numpy().astype(np.float64)))
