@@ -70,6 +70,97 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
   return fmaf(x * s * (e * s), c2 * fmaf(3.0f * 0.044715f, x * x, 1.0f), s);
 }
 
+// Epilogue of W consecutive columns n..n+W-1 of row m (columns >= N
+// skipped); W = 4 for float32 results, 8 for bfloat16 ones.  vec: every
+// access 16-byte aligned and n + W <= N.
+template <int EPI, bool SPLIT, int W>
+__device__ __forceinline__ void epi_store(const KArgs& P, int split, int64_t c_off, int64_t m, int64_t n,
+                                          float (&v)[W], bool vec) {
+  const int64_t rem = P.N - n;
+  const int ne = vec ? W : (int)(rem < W ? rem : W);
+  if constexpr (SPLIT || EPI == EPI_F32 || EPI == EPI_UPDATE) {
+    static_assert(W == 4, "float32 results go four columns at a time");
+    const f32x4 v4{v[0], v[1], v[2], v[3]};
+    if constexpr (SPLIT) {
+      float* dst = P.partial + (int64_t)split * P.M * P.N + m * P.N + n;
+      if (vec) *reinterpret_cast<f32x4*>(dst) = v4;
+      else for (int e = 0; e < ne; ++e) dst[e] = v[e];
+    } else if constexpr (EPI == EPI_UPDATE) {
+      const int64_t off = m * P.ldc + n;
+      if (vec) apply_update4(P.upd, off, v4);
+      else for (int e = 0; e < ne; ++e) apply_update(P.upd, off + e, v[e]);
+    } else {
+      const int64_t off = c_off + m * P.ldc + n;
+      float* dst = reinterpret_cast<float*>(P.C) + off;
+      const float* aux = reinterpret_cast<const float*>(P.aux);
+      if (vec) {
+        f32x4 o = v4;
+        if (P.bias) o += *reinterpret_cast<const f32x4*>(P.bias + n);
+        if (aux) o += *reinterpret_cast<const f32x4*>(aux + off);
+        *reinterpret_cast<f32x4*>(dst) = o;
+      } else {
+        for (int e = 0; e < ne; ++e) {
+          float o = v[e];
+          if (P.bias) o += P.bias[n + e];
+          if (aux) o += aux[off + e];
+          dst[e] = o;
+        }
+      }
+    }
+  } else {
+    static_assert(W == 8, "bfloat16 results go eight columns at a time");
+    const int64_t off = c_off + m * P.ldc + n;
+    if (P.bias && (EPI == EPI_BF16 || EPI == EPI_GELU)) {
+      if (vec) {
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(P.bias + n);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(P.bias + n + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[e] += b0[e];
+          v[e + 4] += b1[e];
+        }
+      } else {
+        for (int e = 0; e < ne; ++e) v[e] += P.bias[n + e];
+      }
+    }
+    float w[8];
+    if constexpr (EPI == EPI_DGELU) {
+      const bf16_t* pre = reinterpret_cast<const bf16_t*>(P.aux) + off;
+      float f[8];
+      if (vec) {
+        const u32x4 u = *reinterpret_cast<const u32x4*>(pre);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          f[2 * e] = __builtin_bit_cast(float, u[e] << 16);
+          f[2 * e + 1] = __builtin_bit_cast(float, u[e] & 0xffff0000u);
+        }
+      } else {
+        for (int e = 0; e < 8; ++e) f[e] = e < ne ? bf2f(pre[e]) : 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] *= gelu_tanh_grad_f(f[e]);
+    }
+    if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = gelu_tanh_f(v[e]);
+    }
+    bf16_t* dst = reinterpret_cast<bf16_t*>(P.C) + off;
+    bf16_t* dst2 = EPI == EPI_GELU ? reinterpret_cast<bf16_t*>(P.C2) + off : nullptr;
+    if (vec) {
+      *reinterpret_cast<u32x4*>(dst) =
+          u32x4{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])};
+      if (EPI == EPI_GELU)
+        *reinterpret_cast<u32x4*>(dst2) =
+            u32x4{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])};
+    } else {
+      for (int e = 0; e < ne; ++e) {
+        dst[e] = f2bf(v[e]);
+        if (EPI == EPI_GELU) dst2[e] = f2bf(w[e]);
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ pipeline
 // K advances in steps of BKV (32 or 64) through rings of LDS stages (one for
 // the A tiles, one for the B tiles; A may run one stage deeper).  Every
@@ -445,43 +536,51 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   }
 
   // ---- epilogue.  32x32 accumulator layout: lane l, register r holds
-  // row (r/4)*8 + (l/32)*4 + r%4, column l%32 of the 32x32 block.
+  // row (r/4)*8 + (l/32)*4 + r%4, column l%32 of the 32x32 block.  Each block
+  // passes through a wave-private LDS buffer, after which every lane owns EW
+  // consecutive columns of one row (4 for float32 results, 8 for bfloat16):
+  // the outputs and the operands the epilogue reads (bias, residual,
+  // pre-activation, optimizer state) move in 16-byte accesses, consecutive
+  // lanes covering a row's columns contiguously.  LDS requests of one wave
+  // are served in order, so the reads see the wave's own writes without a
+  // barrier.
+  constexpr int EW = (SPLIT || EPI == EPI_F32 || EPI == EPI_UPDATE) ? 4 : 8;
+  constexpr int LDW = 40;  // floats per staged row: rows r and r + 4 sit 32 banks apart
+  static_assert(NW * 32 * LDW * 4 <= SA * A_BYTES + SB * B_BYTES, "staging fits in the stages");
+  __syncthreads();  // every wave has finished reading the stages
+  float* const stg = reinterpret_cast<float*>(smem) + wave * 32 * LDW;
   const int64_t c_off = zo * P.c_outer + zi * P.c_inner;
+  uintptr_t ptrs = (uintptr_t)P.C | (uintptr_t)P.C2 | (uintptr_t)P.aux | (uintptr_t)P.bias |
+                   (uintptr_t)P.partial;
+  if (EPI == EPI_UPDATE)
+    ptrs |= (uintptr_t)P.upd.p | (uintptr_t)P.upd.m | (uintptr_t)P.upd.v | (uintptr_t)P.upd.q |
+            ((uintptr_t)P.upd.p16 << 1);
+  const bool vec = (ptrs & 15) == 0 && ((P.ldc | P.c_outer | P.c_inner | P.N) & 7) == 0;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      const int64_t n = n0 + wn * WN + j * 32 + (lane & 31);
-      if (n >= P.N) continue;
-      float bn = 0.f;
-      if (!SPLIT && P.bias && (EPI == EPI_F32 || EPI == EPI_BF16 || EPI == EPI_GELU)) bn = P.bias[n];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t m = m0 + wm * WM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        if (m >= P.M) continue;
-        float v = acc[i][j][r];
-        if (SPLIT) {
-          P.partial[(int64_t)split * P.M * P.N + m * P.N + n] = v;
-          continue;
+      for (int r = 0; r < 16; ++r)
+        stg[((r >> 2) * 8 + (lane >> 5) * 4 + (r & 3)) * LDW + (lane & 31)] = acc[i][j][r];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int it = 0; it < 16 / EW; ++it) {
+        const int item = lane + 64 * it;  // row item/(32/EW), columns (item%(32/EW))*EW .. +EW-1
+        const int rr = item / (32 / EW), cc = (item % (32 / EW)) * EW;
+        float v[EW];
+#pragma unroll
+        for (int q = 0; q < EW / 4; ++q) {
+          const f32x4 x4 = *reinterpret_cast<const f32x4*>(stg + rr * LDW + cc + 4 * q);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[4 * q + e] = x4[e];
         }
-        const int64_t off = c_off + m * P.ldc + n;
-        if (EPI == EPI_F32) {
-          v += bn;
-          if (P.aux) v += reinterpret_cast<const float*>(P.aux)[off];
-          reinterpret_cast<float*>(P.C)[off] = v;
-        } else if (EPI == EPI_BF16) {
-          reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v + bn);
-        } else if (EPI == EPI_GELU) {
-          v += bn;
-          reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v);
-          reinterpret_cast<bf16_t*>(P.C2)[off] = f2bf(gelu_tanh_f(v));
-        } else if (EPI == EPI_UPDATE) {
-          apply_update(P.upd, m * P.ldc + n, v);
-        } else {  // EPI_DGELU
-          float f = bf2f(reinterpret_cast<const bf16_t*>(P.aux)[off]);
-          reinterpret_cast<bf16_t*>(P.C)[off] = f2bf(v * gelu_tanh_grad_f(f));
-        }
+        const int64_t m = m0 + wm * WM + i * 32 + rr;
+        const int64_t n = n0 + wn * WN + j * 32 + cc;
+        if (m < P.M && n < P.N)
+          epi_store<EPI, SPLIT, EW>(P, split, c_off, m, n, v, vec && n + EW <= P.N);
       }
+      __builtin_amdgcn_wave_barrier();
     }
   }
 }
@@ -711,7 +810,9 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
     return (int)std::max<int64_t>(1, std::min<int64_t>(slots / t, max_split));
   };
   if (g.N <= 64) return launch_gemm_bf16_cfg(g, 2, 1, s);
-  if (g.M >= 2048 && g.N >= 2048 && g.K >= 4096 && tiles(256, 256) >= 256)
+  // 256x256 tiles: long K with at least one round of tiles, or enough tiles
+  // (four rounds) for any K (the tied head's forward product)
+  if (g.M >= 2048 && g.N >= 2048 && tiles(256, 256) >= 256 && (g.K >= 4096 || tiles(256, 256) >= 1024))
     return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
   if (splittable && g.K >= 16384 && g.a_kmajor) return launch_gemm_bf16_cfg(g, 4, (int)max_split, s);
   const int64_t t = tiles(128, 128);
