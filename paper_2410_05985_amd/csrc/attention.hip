@@ -43,6 +43,11 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 constexpr int AT_WAVES = 4;              // waves per workgroup, 32 rows each
 constexpr int AT_THREADS = 64 * AT_WAVES;
 constexpr int AT_STEP = 64;              // rows of the walked operand per step (two sub-tiles)
+// Workgroups per CU each kernel is compiled for (the register budget per
+// lane is 512 / occupancy); the LDS of that many workgroups fits in 160 KB.
+#define AT_OCC_FWD(DH) ((DH) <= 64 ? 3 : 2)
+#define AT_OCC_DQ(DH) ((DH) <= 64 ? 3 : 1)
+#define AT_OCC_DKV(DH) ((DH) <= 64 ? 2 : 1)
 
 // LDS tile of AT_STEP rows x DH columns (rows of 2*DH bytes) in one of two
 // layouts, both swizzling 16-byte chunks within a row:
@@ -225,7 +230,7 @@ __device__ __forceinline__ void store_rows(const f32x16 (&acc)[DB], float mul, b
 
 // ---- forward
 template <int DH>
-__global__ __launch_bounds__(AT_THREADS) void attn_fwd_kernel(const bf16_t* __restrict__ qkv,
+__global__ __launch_bounds__(AT_THREADS, AT_OCC_FWD(DH)) void attn_fwd_kernel(const bf16_t* __restrict__ qkv,
                                                               bf16_t* __restrict__ O,
                                                               float* __restrict__ Of,
                                                               float* __restrict__ lse, int B, int H,
@@ -334,7 +339,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_fwd_kernel(const bf16_t* __re
 
 // ---- backward (1): dQ and D, per block of queries
 template <int DH>
-__global__ __launch_bounds__(AT_THREADS) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(AT_THREADS, AT_OCC_DQ(DH)) void attn_bwd_dq_kernel(
     const bf16_t* __restrict__ qkv, const float* __restrict__ lse, const bf16_t* __restrict__ dO,
     const float* __restrict__ Of, float* __restrict__ Dout, bf16_t* __restrict__ dqkv, int B, int H,
     int T, float scale) {
@@ -441,7 +446,7 @@ __global__ __launch_bounds__(AT_THREADS) void attn_bwd_dq_kernel(
 
 // ---- backward (2): dK and dV, per block of keys
 template <int DH>
-__global__ __launch_bounds__(AT_THREADS) void attn_bwd_dkv_kernel(
+__global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kernel(
     const bf16_t* __restrict__ qkv, const float* __restrict__ lse, const bf16_t* __restrict__ dO,
     const float* __restrict__ Din, bf16_t* __restrict__ dqkv, int B, int H, int T, float scale) {
   constexpr int KS = DH / 16, DB = DH / 32, TB = AT_STEP * DH * 2;
