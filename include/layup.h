@@ -376,6 +376,14 @@ typedef struct {
                              deterministic; with and without a workspace the
                              summation order, and so the rounding, differ. */
   size_t workspace_bytes;
+  float* a_rowsum;        /* device, optional (bf16 path, a_kmajor = 0, batch
+                             1): a_rowsum[m] = sum over k of A(m, k) in
+                             float32, accumulated by the same kernel from
+                             the A operand it multiplies -- for the dW GEMM
+                             of a linear layer (A = dY^T) the bias gradient
+                             db = column sums of dY (Algorithm 1, backward
+                             pass).  With split-K the workspace also holds
+                             one float per row per split. */
 } layup_gemm_desc;
 
 layup_status layup_gemm_bf16(const layup_gemm_desc* d, void* stream);

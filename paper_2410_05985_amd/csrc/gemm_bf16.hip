@@ -44,6 +44,7 @@ struct KArgs {
   int32_t causal, nz;      // nz: batch count
   int64_t k_per_split;
   UpdArgs upd;             // EPI_UPDATE
+  float* rowsum;           // row sums of an m-major A (split-K: partials after the C partials)
 };
 
 // GELU, tanh form: 0.5 x (1 + tanh(u)), u = sqrt(2/pi) (x + 0.044715 x^3).
@@ -68,6 +69,18 @@ __device__ __forceinline__ float gelu_tanh_grad_f(float x) {
   const float s = gelu_sig(x, e);
   const float c2 = 2.0f * 0.7978845608028654f;
   return fmaf(x * s * (e * s), c2 * fmaf(3.0f * 0.044715f, x * x, 1.0f), s);
+}
+
+// Sum of the 8 bfloat16 values of an MFMA operand register quad, in order.
+__device__ __forceinline__ float sum_bf16x8(const u32x4& u) {
+  float s = __builtin_bit_cast(float, u[0] << 16);
+  s += __builtin_bit_cast(float, u[0] & 0xffff0000u);
+#pragma unroll
+  for (int e = 1; e < 4; ++e) {
+    s += __builtin_bit_cast(float, u[e] << 16);
+    s += __builtin_bit_cast(float, u[e] & 0xffff0000u);
+  }
+  return s;
 }
 
 // Epilogue of W consecutive columns n..n+W-1 of row m (columns >= N
@@ -413,6 +426,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
+  // Row sums of an m-major A (bias gradient of dW = dY^T X): the waves of
+  // the first wave column in the first tile column add up the A fragments
+  // they feed to the MFMAs (lane l: row l % 32 of block i, 8 of every 16 k).
+  const bool rs_on = !AK && P.rowsum && tn == 0 && wn == 0;
+  float rsum[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) rsum[i] = 0.f;
+
   // per-lane fragment offsets inside a stage (B after A)
   constexpr int NA = AK ? KS : TM, NB = BKM ? KS : TN;
   uint32_t a_off[NA], b_off[NB];
@@ -526,6 +547,12 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, af[cb][i]),
                                                               __builtin_bit_cast(bf16x8, bfr[cb][j]),
                                                               acc[i][j], 0, 0, 0);
+      if constexpr (!AK) {
+        if (rs_on) {
+#pragma unroll
+          for (int i = 0; i < TM; ++i) rsum[i] += sum_bf16x8(af[cb][i]);
+        }
+      }
       // deep pipelines: this sub-step's share of the next stage's copies,
       // whose address arithmetic runs while the MFMAs just issued execute
       if constexpr (SPREAD) {
@@ -545,6 +572,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   // are served in order, so the reads see the wave's own writes without a
   // barrier.
   constexpr int EW = (SPLIT || EPI == EPI_F32 || EPI == EPI_UPDATE) ? 4 : 8;
+  if constexpr (!AK) {
+    if (rs_on) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const float tot = rsum[i] + __shfl_xor(rsum[i], 32, 64);  // the two k halves
+        const int64_t m = m0 + wm * WM + i * 32 + lane;
+        if (lane < 32 && m < P.M) {
+          if (SPLIT) P.partial[(int64_t)P.splits * P.M * P.N + (int64_t)split * P.M + m] = tot;
+          else P.rowsum[m] = tot;
+        }
+      }
+    }
+  }
   constexpr int LDW = 40;  // floats per staged row: rows r and r + 4 sit 32 banks apart
   static_assert(NW * 32 * LDW * 4 <= SA * A_BYTES + SB * B_BYTES, "staging fits in the stages");
   __syncthreads();  // every wave has finished reading the stages
@@ -596,6 +636,12 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
   const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (n >= P.N) return;
   const int64_t total = P.M * P.N;
+  if (P.rowsum && blockIdx.x == 0 && threadIdx.x == 0) {
+    const float* rp = P.partial + P.splits * total + m;
+    float r = rp[0];
+    for (int s = 1; s < P.splits; ++s) r += rp[(int64_t)s * P.M];
+    P.rowsum[m] = r;
+  }
   const float* src = P.partial + m * P.N + n;
   if (EPI == EPI_UPDATE) {
     const int64_t off = m * P.ldc + n;
@@ -707,6 +753,7 @@ KArgs make_args(const Gemm& g) {
   P.causal = g.causal;
   P.nz = g.batch;
   P.upd = g.upd;
+  P.rowsum = g.rowsum;
   return P;
 }
 
@@ -721,6 +768,7 @@ std::string gemm_check(const Gemm& g, bool f32_operands) {
     if (!g.upd.p || !g.upd.m || !g.upd.q || (g.upd.adamw && !g.upd.v)) return "update epilogue needs p, m, (v) and q";
     if (g.a_kmajor || g.b_kmajor || g.batch != 1) return "update epilogue only for dW = dY^T X";
   }
+  if (g.rowsum && (g.a_kmajor || g.batch != 1)) return "row sums of A only for an m-major A, batch 1";
   if (g.epi == EPI_GELU && !g.C2) return "GELU epilogue needs a second output";
   if (g.epi == EPI_DGELU && !g.aux) return "GELU-backward epilogue needs the pre-activation";
   const int64_t a_contig0 = g.a_kmajor ? g.K : g.M;
@@ -762,7 +810,8 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
   P.tiles_m = (int)cdiv(g.M, BM);
   P.tiles_n = (int)cdiv(g.N, BN);
   if (splits > 1 && g.batch == 1 && g.splitk_ws && (g.epi == EPI_F32 || g.epi == EPI_UPDATE) && g.M <= 65535) {
-    while (splits > 1 && (size_t)splits * g.M * g.N * 4 > g.splitk_ws_bytes) --splits;
+    const size_t per_split = (size_t)g.M * g.N * 4 + (g.rowsum ? (size_t)g.M * 4 : 0);
+    while (splits > 1 && splits * per_split > g.splitk_ws_bytes) --splits;
     if (splits > 1) {
       P.k_per_split = cdiv(cdiv(g.K, splits), 32) * 32;
       P.splits = (int)cdiv(g.K, P.k_per_split);

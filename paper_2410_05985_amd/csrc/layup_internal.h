@@ -145,6 +145,9 @@ struct Gemm {
   //   CAUSAL_A_UPPER: A(m, k) = 0 for k < m (P^T dO, dS^T Q): K starts at the tile's first row.
   int causal = 0;
   UpdArgs upd{};  // EPI_UPDATE
+  // m-major A only (dW = dY^T X): rowsum[m] = sum over k of A(m, k), the
+  // bias gradient, accumulated from the A fragments the MFMAs consume
+  float* rowsum = nullptr;
 };
 enum Causal : int { CAUSAL_NONE = 0, CAUSAL_OUT_LOWER = 1, CAUSAL_A_LOWER = 2, CAUSAL_A_UPPER = 3 };
 

@@ -201,10 +201,9 @@ struct layup_ctx {
   // ev_rd[k][p]: its dW GEMM and bias sum done (update stream);
   // ev_dx: a dX GEMM issued (fused schedule: dW runs after it)
   hipEvent_t ev_wr[4][2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
-  float *ln_part = nullptr, *cs_part = nullptr, *cs_part_su = nullptr;
+  float *ln_part = nullptr, *cs_part = nullptr;
   int64_t cs_part_floats = 0;
   ColsumScratch cs() const { return ColsumScratch{cs_part, cs_part_floats}; }
-  ColsumScratch cs_su() const { return ColsumScratch{cs_part_su, cs_part_floats}; }
   float *splitk = nullptr, *splitk_su = nullptr;
   size_t splitk_bytes = 0, splitk_su_bytes = 0;
   bool dw_side() const { return su != sc; }
@@ -270,9 +269,6 @@ size_t carve(layup_ctx* c, char* base) {
     }
     c->do16 = cv.take<bf16_t>(N * d);
     c->ln_part = cv.take<float>(layernorm_bwd_partial_floats(N, (int)d));
-    c->cs_part_floats = cdiv(N, 128) * std::max<int64_t>(3 * d, F);
-    c->cs_part = cv.take<float>(c->cs_part_floats);
-    c->cs_part_su = cv.take<float>(c->cs_part_floats);
     c->splitk = cv.take<float>(SPLITK_BYTES / 4);
     c->splitk_bytes = SPLITK_BYTES;
     c->splitk_su = cv.take<float>(SPLITK_SU_BYTES / 4);
@@ -514,15 +510,17 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   // dW and db.  In the fused schedule the dW GEMM updates the weight in
   // place, so it waits for the layer's dX (which reads the weight first).
   const bool fz = c->fused_dw;
-  auto weight_grads = [&](int op, Gemm dw, const std::string& wname, const bf16_t* dy, int64_t cols,
-                          const char* bname, const char* what, const char* bwhat) -> layup_status {
+  // The bias gradient (column sums of dY) comes out of the same dW GEMM: its
+  // A operand is dY^T, whose row sums it accumulates from the fragments.
+  auto weight_grads = [&](int op, Gemm dw, const std::string& wname, const char* bname,
+                          const char* what) -> layup_status {
     HIPCHK(c, wait(sw, c->ev_wr[op][pq]), "wait operand written");
     if (fz) {
       HIPCHK(c, rec(c->ev_dx, s), "record dX issued");
       HIPCHK(c, wait(sw, c->ev_dx), "wait dX");
     }
+    dw.rowsum = fl.g(p + bname);
     TRY(run_gemm(c, dw_gemm(c, dw, wname), sw, what, true));
-    HIPCHK(c, launch_colsum_bf16(dy, N, cols, cols, side ? c->cs_su() : c->cs(), fl.g(p + bname), sw), bwhat);
     HIPCHK(c, rec(c->ev_rd[op][pq], sw), "record operand read");
     return LAYUP_OK;
   };
@@ -533,12 +531,12 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
   HIPCHK(c, rec(c->ev_wr[OP_F][pq], s), "record operand written");
   TRY(weight_grads(OP_A, mk(false, false, d, F, N, dyA, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
-                   p + "mproj.w", dyA, d, "mproj.b", "mproj dW", "mproj db"));
+                   p + "mproj.w", "mproj.b", "mproj dW + db"));
   // MLP input projection: dY = df16
   Gemm fcx = mk(true, false, N, d, F, df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
   TRY(run_gemm(c, fcx, s, "fc dX", true));
   TRY(weight_grads(OP_F, mk(false, false, F, d, N, df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
-                   p + "fc.w", df16, F, "fc.b", "fc dW", "fc db"));
+                   p + "fc.w", "fc.b", "fc dW + db"));
   HIPCHK(c, wait(s, c->ev_rd[OP_B][pq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
                                  dyB, c->ln_part, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
@@ -548,7 +546,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   Gemm prx = mk(true, false, N, d, d, dyB, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
   TRY(run_gemm(c, prx, s, "proj dX", true));
   TRY(weight_grads(OP_B, mk(false, false, d, d, N, dyB, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32),
-                   p + "proj.w", dyB, d, "proj.b", "proj dW", "proj db"));
+                   p + "proj.w", "proj.b", "proj dW + db"));
   HIPCHK(c, wait(s, c->ev_rd[OP_Q][pq]), "wait operand free");
   if (A.of) {
     // attention core, fused: dQ, dK, dV from recomputed scores (P and dS stay
@@ -590,7 +588,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   Gemm qx = mk(true, false, N, d, 3 * d, dq16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
   TRY(run_gemm(c, qx, s, "qkv dX", true));
   TRY(weight_grads(OP_Q, mk(false, false, 3 * d, d, N, dq16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d, EPI_F32),
-                   p + "qkv.w", dq16, 3 * d, "qkv.b", "qkv dW", "qkv db"));
+                   p + "qkv.w", "qkv.b", "qkv dW + db"));
   // LayerNorm 1; its bf16 dx is the next block's output-gradient operand
   const int nq = pq ^ 1;
   if (l > 0) HIPCHK(c, wait(s, c->ev_rd[OP_A][nq]), "wait operand free");
@@ -1203,6 +1201,8 @@ static layup_status gemm_abi(const layup_gemm_desc* d, void* stream, bool f32) {
   g.epi = (f32 || d->c_f32) ? EPI_F32 : EPI_BF16;
   g.splitk_ws = (float*)d->workspace;
   g.splitk_ws_bytes = d->workspace_bytes;
+  g.rowsum = d->a_rowsum;
+  if (f32 && d->a_rowsum) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "row sums of A only on the bf16 path");
   if (f32 && !d->c_f32) return fail(nullptr, LAYUP_ERR_DTYPE, "the float32 GEMM writes float32");
   if (f32 && g.batch != 1) return fail(nullptr, LAYUP_ERR_SHAPE, "the float32 GEMM is not batched");
   if (d->workspace && ((uintptr_t)d->workspace & 15)) return fail(nullptr, LAYUP_ERR_ALIGN, "workspace must be 16-byte aligned");

@@ -77,7 +77,8 @@ class layup_gemm_desc(C.Structure):
                 ("bias", C.c_void_p),
                 ("a_outer", C.c_int64), ("a_inner", C.c_int64), ("b_outer", C.c_int64),
                 ("b_inner", C.c_int64), ("c_outer", C.c_int64), ("c_inner", C.c_int64),
-                ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
+                ("a_rowsum", C.c_void_p)]
 
 
 # exported names, in header order
@@ -322,7 +323,7 @@ def layup_activation(ctx, which: int, layer: int = 0):
 
 def gemm_desc(A, B, C_, M, N, K, lda, ldb, ldc, a_kmajor=True, b_kmajor=True, c_f32=True,
               bias=None, batch=1, inner=1, a_strides=(0, 0), b_strides=(0, 0), c_strides=(0, 0),
-              workspace=None, workspace_bytes=0) -> layup_gemm_desc:
+              workspace=None, workspace_bytes=0, a_rowsum=None) -> layup_gemm_desc:
     d = layup_gemm_desc()
     d.a_kmajor, d.b_kmajor = int(a_kmajor), int(b_kmajor)
     d.M, d.N, d.K = M, N, K
@@ -333,6 +334,7 @@ def gemm_desc(A, B, C_, M, N, K, lda, ldb, ldc, a_kmajor=True, b_kmajor=True, c_
     d.b_outer, d.b_inner = b_strides
     d.c_outer, d.c_inner = c_strides
     d.workspace, d.workspace_bytes = _ptr(workspace), workspace_bytes
+    d.a_rowsum = _ptr(a_rowsum)
     return d
 
 

@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 from paper_2410_05985_amd import synthetic as S
+import oracle as O
 from tests.parity import compare
 
 pytestmark = pytest.mark.gpu
@@ -94,6 +95,38 @@ def test_gemm_dw_many_tiles():
     got, ref = run("mn", 4096, 2200, 200, seed=17)
     compare(got, ref, 2e-2, "dW many tiles")
     assert np.linalg.norm(got - ref) <= 1e-4 * np.linalg.norm(ref)
+
+
+@pytest.mark.parametrize("M,N,K,ws", [(256, 384, 192, False), (200, 136, 72, False),
+                                      (256, 256, 8192, True), (520, 264, 3000, True),
+                                      (2304, 768, 8192, True)])
+def test_gemm_dw_bias_row_sums(M, N, K, ws):
+    """dW = dY^T X with the bias gradient db = column sums of dY accumulated
+    by the same kernel (a_rowsum), with and without split-K (ragged shapes):
+    both against the oracle's linear-layer backward of the same bf16 values,
+    db at 1e-4 (float32 sums of K terms)."""
+    A = bf16_tensor((K, M), 41 + M, 0.5)   # dY, tokens x out
+    B = bf16_tensor((K, N), 42 + N, 0.5)   # X, tokens x in
+    dy, x = as_f64(A), as_f64(B)
+    dw_ref, db_ref, _ = O.linear_bwd(dy, x, None, need_dx=False)
+    Cd = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    db = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV)
+    w = torch.empty(64 << 20, dtype=torch.uint8, device=DEV) if ws else None
+    d = LU.gemm_desc(A.to(DEV), B.to(DEV), Cd, M, N, K, M, N, N, False, False, True,
+                     workspace=w, workspace_bytes=(64 << 20) if ws else 0, a_rowsum=db)
+    LU.layup_gemm_bf16(d, torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    compare(Cd.cpu().numpy(), dw_ref, 2e-2, f"dW {M}x{N}x{K}")
+    compare(db.cpu().numpy(), db_ref, 1e-4, f"db {M}x{N}x{K}")
+
+
+def test_gemm_row_sums_need_m_major_a():
+    A = bf16_tensor((64, 64), 1).to(DEV)
+    Cd = torch.empty((64, 64), dtype=torch.float32, device=DEV)
+    db = torch.empty(64, dtype=torch.float32, device=DEV)
+    d = LU.gemm_desc(A, A, Cd, 64, 64, 64, 64, 64, 64, True, False, True, a_rowsum=db)
+    with pytest.raises(RuntimeError):
+        LU.layup_gemm_bf16(d, torch.cuda.current_stream())
 
 
 def test_gemm_batched_attention_strides():
