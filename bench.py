@@ -22,6 +22,10 @@ Other workloads (one JSON line each, not the default bench line):
   --workload mlp           tiny float32 MLP, 10 layer-wise steps
   --workload gossip        4 GPT-2-small replicas resident on the GPU taking
                            steps in turn, push mode with push-sum weights
+  --workload gemm-yardstick  the backward GEMM shapes of a GPT-2-small block,
+                           its tied head and a 1.3B block, each timed with
+                           this library's GEMM and with torch.matmul
+                           (hipBLASLt) on the same operands, cold operands
   --workload kernels       one launch each of: a 1 GiB copy (counter
                            calibration), one GPT-2-small block's 8 backward
                            GEMMs, one block's update+mix -- for rocprofv3 --pmc
@@ -59,7 +63,7 @@ def parse():
     ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
     ap.add_argument("--workload", default="gpt2-small",
                     choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp",
-                             "gossip", "kernels"])
+                             "gossip", "kernels", "gemm-yardstick"])
     return ap.parse_args()
 
 
@@ -448,6 +452,55 @@ def bench_gossip(args, torch, LU, S):
         mk.close()
 
 
+def time_torch_mm(torch, shapes, reps, stream, cold_bytes=512 << 20):
+    """torch.matmul (hipBLASLt) on the layouts of time_gemms: C = A B with A
+    [M, K] (a_kmajor) or the transpose of a [K, M] array, B [K, N] (b not
+    k-major) or the transpose of [N, K].  bf16 in, bf16 out (torch has no
+    float32-output bf16 matmul), operands rotated as in time_gemms."""
+    res = []
+    for name, M, N, K, ak, bk in shapes:
+        per = 2 * M * K + 2 * N * K + 2 * M * N
+        R = max(1, min(16, -(-cold_bytes // per)))
+        ops = []
+        for _ in range(R):
+            A = torch.randn((M, K) if ak else (K, M), device="cuda").to(torch.bfloat16)
+            B = torch.randn((N, K) if bk else (K, N), device="cuda").to(torch.bfloat16)
+            ops.append((A if ak else A.t(), B.t() if bk else B))
+        with torch.cuda.stream(stream):
+            for a, b in ops:
+                torch.matmul(a, b)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for r in range(reps):
+                a, b = ops[r % R]
+                torch.matmul(a, b)
+            e1.record(stream)
+        e1.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        res.append(dict(name=name, ms=ms, tflops=2.0 * M * N * K / (ms * 1e-3) / 1e12))
+        del ops
+    return res
+
+
+def bench_gemm_yardstick(args, torch, LU, S):
+    """This library's GEMM next to hipBLASLt on the backward shapes: one
+    GPT-2-small block and its tied head, and one 1.3B block."""
+    stream = torch.cuda.Stream()
+    rows = []
+    for tag, cfg in (("gpt2-small", S.GPT2_SMALL), ("gpt-1.3b", S.GPT_1P3B)):
+        blk, head = backward_gemm_shapes(cfg)
+        shapes = blk + (head if tag == "gpt2-small" else [])
+        ours = time_gemms(torch, LU, shapes, args.kernel_reps, stream)
+        ref = time_torch_mm(torch, shapes, args.kernel_reps, stream)
+        for (name, M, N, K, ak, bk), o, r in zip(shapes, ours, ref):
+            rows.append(dict(config=tag, gemm=name, M=M, N=N, K=K, ours_us=round(o["ms"] * 1e3, 1),
+                             ours_tflops=round(o["tflops"], 1), hipblaslt_us=round(r["ms"] * 1e3, 1),
+                             hipblaslt_tflops=round(r["tflops"], 1)))
+    print(json.dumps({"workload": "gemm-yardstick", "peak_tflops": PEAK_BF16_TFLOPS, "gemms": rows,
+                      "note": "ours: float32 output (dW, dX as in the step); hipBLASLt: bf16 output"}),
+          flush=True)
+
+
 def bench_kernels(args, torch, LU, S):
     """Single launches for hardware-counter runs, in this order: a 1 GiB
     device copy (known traffic: 1 GiB read + 1 GiB written), the 8 backward
@@ -508,6 +561,8 @@ def main():
             bench_mlp(args, torch, LU, S)
         elif args.workload == "gossip":
             bench_gossip(args, torch, LU, S)
+        elif args.workload == "gemm-yardstick":
+            bench_gemm_yardstick(args, torch, LU, S)
         else:
             bench_gpt_other(args, torch, LU, S, args.workload)
         return
