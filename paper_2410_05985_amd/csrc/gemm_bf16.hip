@@ -828,18 +828,22 @@ hipError_t launch_gemm_bf16_cfg(const Gemm& g, int cfg, int splits, hipStream_t 
   }
 }
 
-// Tile choice (measured on the GPT-2-small shapes with operands arriving from
-// HBM, as inside the step):
+// Tile choice (measured on the GPT-2-small shapes with random operands
+// arriving from HBM, as inside the step -- under the power limit the clock,
+// and so the ranking, depends on the data):
 //  - N <= 64 (attention head width): 128x64;
 //  - both output dimensions >= 2048, K >= 4096 and at least 256 tiles:
 //    256x256 with K steps of 64;
 //  - float32 output and K >= 16384 (the tied head's dX over the vocabulary):
 //    256x256 with four stages of K 32 and an 8-way split of K;
+//  - dW = dY^T X with at least 256 tiles of 256x256 (the head's dW): 256x256
+//    with K steps of 64;
 //  - float32 outputs with an m-major B (dX = dY W, and dW = dY^T X with fewer
 //    than 512 tiles) and float32 forward products: 128x128 with K steps of
 //    64, two workgroups per CU; for m-major B, split-K fills the 512
 //    workgroup slots of one round (largest split with tiles x split <= 512);
-//  - dW with at least 512 tiles (the head's dW): 256x128, three stages of K 32;
+//  - dW with at least 512 tiles of 128x128 otherwise: 256x128, three stages
+//    of K 32;
 //  - otherwise (forward products with bf16/GELU epilogues): 128x128 with K
 //    steps of 32 and three stages (more loads in flight for short K).
 // Split-K (float32 partials, fixed-order sum) only with K >= 1536, at least
@@ -864,6 +868,7 @@ hipError_t launch_gemm_bf16(const Gemm& g, hipStream_t s) {
   if (g.M >= 2048 && g.N >= 2048 && tiles(256, 256) >= 256 && (g.K >= 4096 || tiles(256, 256) >= 1024))
     return launch_gemm_bf16_cfg(g, 0, split_for(tiles(256, 256), 256), s);
   if (splittable && g.K >= 16384 && g.a_kmajor) return launch_gemm_bf16_cfg(g, 4, (int)max_split, s);
+  if (f32_out && !g.a_kmajor && !g.b_kmajor && tiles(256, 256) >= 256) return launch_gemm_bf16_cfg(g, 0, 1, s);
   const int64_t t = tiles(128, 128);
   if (f32_out && !g.b_kmajor && (g.a_kmajor || t < 512)) return launch_gemm_bf16_cfg(g, 3, fill_split(t, 512), s);
   if (f32_out && g.a_kmajor && g.b_kmajor) return launch_gemm_bf16_cfg(g, 3, 1, s);
