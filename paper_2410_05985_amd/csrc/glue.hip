@@ -118,7 +118,9 @@ hipError_t launch_embed_bwd(const float* dx, const int32_t* sorted_pos, float* d
 // ------------------------------------------------------------- LayerNorm
 // One wave64 per row, 4 rows per block.  y = (x - mean) * rstd * g + b in
 // bf16; mean and rstd (1/sqrt(var + 1e-5), biased variance) kept for the
-// backward.
+// backward.  The row is read once into registers (NVL float4 groups per
+// lane, d <= 256*NVL); the mean and the variance are two passes over them.
+template <int NVL>
 __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, const float* g,
                                                             const float* b, bf16_t* y,
                                                             float* mean, float* rstd,
@@ -128,30 +130,38 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, cons
   if (row >= rows) return;
   const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * d);
   const int nv = d / 4;
-  float s = 0.f;
-  for (int i = lane; i < nv; i += 64) {
-    f32x4 v = xr[i];
-    s += (v[0] + v[1]) + (v[2] + v[3]);
+  f32x4 v[NVL];
+#pragma unroll
+  for (int j = 0; j < NVL; ++j) {
+    const int i = lane + 64 * j;
+    if (i < nv) v[j] = xr[i];
   }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NVL; ++j)
+    if (lane + 64 * j < nv) s += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
   const float mu = warp_sum(s) / d;
   float ss = 0.f;
-  for (int i = lane; i < nv; i += 64) {
-    f32x4 v = xr[i];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float c = v[j] - mu;
+  for (int j = 0; j < NVL; ++j) {
+    if (lane + 64 * j >= nv) continue;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float c = v[j][e] - mu;
       ss = fmaf(c, c, ss);
     }
   }
   const float var = warp_sum(ss) / d;
   const float r = 1.0f / sqrtf(var + 1e-5f);
-  for (int i = lane; i < nv; i += 64) {
-    f32x4 v = xr[i];
-    f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
-    f32x4 bb = reinterpret_cast<const f32x4*>(b)[i];
+#pragma unroll
+  for (int j = 0; j < NVL; ++j) {
+    const int i = lane + 64 * j;
+    if (i >= nv) continue;
+    const f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
+    const f32x4 bb = reinterpret_cast<const f32x4*>(b)[i];
     u32x2 o;
-    o[0] = pack_bf2((v[0] - mu) * r * gg[0] + bb[0], (v[1] - mu) * r * gg[1] + bb[1]);
-    o[1] = pack_bf2((v[2] - mu) * r * gg[2] + bb[2], (v[3] - mu) * r * gg[3] + bb[3]);
+    o[0] = pack_bf2((v[j][0] - mu) * r * gg[0] + bb[0], (v[j][1] - mu) * r * gg[1] + bb[1]);
+    o[1] = pack_bf2((v[j][2] - mu) * r * gg[2] + bb[2], (v[j][3] - mu) * r * gg[3] + bb[3]);
     reinterpret_cast<u32x2*>(y + row * d)[i] = o;
   }
   if (lane == 0) {
@@ -162,7 +172,14 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, cons
 
 hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, bf16_t* y,
                                 float* mean, float* rstd, int64_t rows, int d, hipStream_t s) {
-  layernorm_fwd_kernel<<<(unsigned)cdiv(rows, 4), 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  if (d % 4 != 0 || d > 256 * 8 || rows <= 0) return hipErrorInvalidValue;
+  const unsigned nb = (unsigned)cdiv(rows, 4);
+  const int nvl = (int)cdiv(d / 4, 64);
+  if (nvl <= 1) layernorm_fwd_kernel<1><<<nb, 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  else if (nvl == 2) layernorm_fwd_kernel<2><<<nb, 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  else if (nvl == 3) layernorm_fwd_kernel<3><<<nb, 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  else if (nvl == 4) layernorm_fwd_kernel<4><<<nb, 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
+  else layernorm_fwd_kernel<8><<<nb, 256, 0, s>>>(x, g, b, y, mean, rstd, rows, d);
   return hipGetLastError();
 }
 
@@ -703,18 +720,24 @@ __global__ void mean_kernel(const float* x, int64_t n, float* out) {
 }
 
 // Register-resident form for rows of at most CE_T x CE_CH 16-byte vectors
-// (V <= 53248; wider rows take ce_kernel): each of CE_T threads loads its vectors once (all loads in
-// flight together), so the row is read from HBM once; the exponentials are
-// cheap (exp_acc) and taken again for the gradient.  The maximum is exact;
-// the sum of e^(z - max) is accumulated in double precision in a fixed order
-// (per thread, then a shuffle tree, then the waves in order), so the
-// normaliser is within about an ulp of the exact one.  Deterministic.
+// (V <= 53248; wider rows take ce_kernel): each of CE_T threads loads its
+// vectors once (all loads in flight together), so the row is read from HBM
+// once.  The maximum M is exact.  e^(z - M) is taken as 2^(z log2(e) - Ms)
+// with Ms = M log2(e) rounded to float: one fused multiply-add and the
+// hardware exponential per element; the rounding of Ms scales every term by
+// the same factor c, which cancels in the probabilities and is removed from
+// the loss (log c computed in double precision).  The sum is accumulated in
+// double precision in a fixed order (per thread, a shuffle tree, the waves
+// in order).  Only vectors that reach past V test each column.  The
+// exponentials are taken again for the gradient; the target's -1 is
+// applied by the one thread holding it.  Deterministic.
 constexpr int CE_T = 512;
 template <int CE_CH>
 __global__ __launch_bounds__(CE_T) void ce_regs_kernel(const bf16_t* z, int64_t ld, const int32_t* tokens,
                                                        int T, int V, int64_t n_rows, bf16_t* dz,
                                                        float* loss_rows) {
   constexpr int NW = CE_T / 64;
+  constexpr float L2E = 1.4426950408889634f;
   __shared__ float rmax[NW];
   __shared__ double rsum[NW];
   const int64_t row = blockIdx.x;
@@ -731,62 +754,76 @@ __global__ __launch_bounds__(CE_T) void ce_regs_kernel(const bf16_t* z, int64_t 
     const int v = threadIdx.x + CE_T * c;
     if (v < nv) w[c] = zr[v];
   }
-  auto val = [&](int c, int e) {  // element e of this thread's vector c, -inf past V
-    const int j = 8 * (threadIdx.x + CE_T * c) + e;
+  auto raw = [&](int c, int e) {  // element e of this thread's vector c
     const uint32_t u = w[c][e >> 1];
-    const float x = __builtin_bit_cast(float, (e & 1) ? (u & 0xffff0000u) : (u << 16));
-    return j < V ? x : -INFINITY;
+    return __builtin_bit_cast(float, (e & 1) ? (u & 0xffff0000u) : (u << 16));
   };
   float m = -INFINITY;
 #pragma unroll
-  for (int c = 0; c < CE_CH; ++c)
-    if (threadIdx.x + CE_T * c < nv)
+  for (int c = 0; c < CE_CH; ++c) {
+    const int v = threadIdx.x + CE_T * c;
+    if (v >= nv) continue;
+    if (8 * v + 8 <= V) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) m = fmaxf(m, val(c, e));
+      for (int e = 0; e < 8; ++e) m = fmaxf(m, raw(c, e));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (8 * v + e < V) m = fmaxf(m, raw(c, e));
+    }
+  }
   m = warp_max(m);
   if ((threadIdx.x & 63) == 0) rmax[threadIdx.x >> 6] = m;
   __syncthreads();
   float M = rmax[0];
 #pragma unroll
   for (int q = 1; q < NW; ++q) M = fmaxf(M, rmax[q]);
-  // e^(z - max), 0 past V; taken again (bitwise the same) for the gradient
-  auto prob = [&](int c, int e) {
-    const float x = val(c, e);
-    return x == -INFINITY ? 0.f : exp_acc(x - M);
+  const float Ms = M * L2E;
+  // c * e^(z - M) for column j < V (bitwise the same in both uses), 0 past V
+  auto prob = [&](int c, int e, bool full) {
+    const int j = 8 * (threadIdx.x + CE_T * c) + e;
+    const float p = __builtin_amdgcn_exp2f(fmaf(raw(c, e), L2E, -Ms));
+    return (full || j < V) ? p : 0.f;
   };
   double sum = 0.0;
 #pragma unroll
-  for (int c = 0; c < CE_CH; ++c)
-    if (threadIdx.x + CE_T * c < nv)
+  for (int c = 0; c < CE_CH; ++c) {
+    const int v = threadIdx.x + CE_T * c;
+    if (v >= nv) continue;
+    const bool full = 8 * v + 8 <= V;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sum += (double)prob(c, e);
+    for (int e = 0; e < 8; ++e) sum += (double)prob(c, e, full);
+  }
   for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
   if ((threadIdx.x & 63) == 0) rsum[threadIdx.x >> 6] = sum;
   __syncthreads();
   double S = 0.0;
 #pragma unroll
   for (int q = 0; q < NW; ++q) S += rsum[q];
-  const float inv = (float)(1.0 / S);
   const float scale = 1.0f / (float)n_rows;
+  const float ks = (float)(1.0 / S) * scale;
   u32x4* dr = reinterpret_cast<u32x4*>(dz + row * ld);
+  const int tv = tgt >> 3, te = tgt & 7;
 #pragma unroll
   for (int c = 0; c < CE_CH; ++c) {
     const int v = threadIdx.x + CE_T * c;
     if (v >= nv) continue;
-    u32x4 o;
+    const bool full = 8 * v + 8 <= V;
+    float g[8];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      float g[2];
+    for (int e = 0; e < 8; ++e) g[e] = valid ? prob(c, e, full) * ks : 0.f;
+    if (valid && v == tv) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int j = 8 * v + 2 * k + h;
-        g[h] = valid ? (prob(c, 2 * k + h) * inv - (j == tgt ? 1.0f : 0.0f)) * scale : 0.f;
-      }
-      o[k] = pack_bf2(g[0], g[1]);
+      for (int e = 0; e < 8; ++e)
+        if (e == te) g[e] -= scale;
     }
-    dr[v] = o;
+    dr[v] = u32x4{pack_bf2(g[0], g[1]), pack_bf2(g[2], g[3]), pack_bf2(g[4], g[5]), pack_bf2(g[6], g[7])};
   }
-  if (threadIdx.x == 0) loss_rows[row] = valid ? (float)(log(S) + (double)M - (double)zt) : 0.0f;
+  if (threadIdx.x == 0) {
+    // S = c * sum e^(z - M) with c = 2^(M log2(e) - Ms)
+    const double log_c = ((double)M * 1.4426950408889634 - (double)Ms) * 0.6931471805599453;
+    loss_rows[row] = valid ? (float)(log(S) - log_c + (double)M - (double)zt) : 0.0f;
+  }
 }
 
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B, int T,
