@@ -159,6 +159,10 @@ __device__ __forceinline__ bf16x8 pack8(const float* v) {
   return __builtin_bit_cast(bf16x8, w);
 }
 
+// The two bfloat16 halves of a packed pair, as floats.
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __builtin_bit_cast(float, u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __builtin_bit_cast(float, u & 0xffff0000u); }
+
 // Key (or query) of accumulator register r for lane half h, relative to the
 // 32-row sub-tile start.
 __device__ __forceinline__ int acc_key(int r, int h) { return (r >> 2) * 8 + 4 * h + (r & 3); }
@@ -284,11 +288,13 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_FWD(DH)) void attn_fwd_kernel(co
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kt, 1, ks, lane), qf[ks], s1, 0, 0, 0);
       }
       const int k0 = st * AT_STEP;
+      // raw scores; the scale c2 > 0 is applied after the maximum (rounding
+      // is monotone, so max(s) c2 = max(s c2)) inside the exponent's fma
       float x[32];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        x[r] = s0[r] * c2;
-        x[16 + r] = s1[r] * c2;
+        x[r] = s0[r];
+        x[16 + r] = s1[r];
       }
       if (k0 + AT_STEP - 1 > qlo || k0 + AT_STEP > T) {  // diagonal or last step: mask
 #pragma unroll
@@ -300,13 +306,13 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_FWD(DH)) void attn_fwd_kernel(co
       float tmax = x[0];
 #pragma unroll
       for (int r = 1; r < 32; ++r) tmax = fmaxf(tmax, x[r]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * c2;
       const float mn = fmaxf(m, tmax);
       const float alpha = __builtin_amdgcn_exp2f(m - mn);  // 0 on the first step
       float ps = 0.f;
 #pragma unroll
       for (int r = 0; r < 32; ++r) {
-        x[r] = __builtin_amdgcn_exp2f(x[r] - mn);
+        x[r] = __builtin_amdgcn_exp2f(fmaf(x[r], c2, -mn));
         ps += x[r];
       }
       l = fmaf(l, alpha, ps);
@@ -379,6 +385,7 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DQ(DH)) void attn_bwd_dq_kernel(
     }
   }
   const float D = part + __shfl_xor(part, 32, 64);
+  const float Ds = D * scale;
   const float ls = lse[z * T + qc];
   if (q < T && h == 0 && it.mine > 0) Dout[z * T + q] = D;
   f32x16 qacc[DB];
@@ -414,16 +421,21 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DQ(DH)) void attn_bwd_dq_kernel(
           sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(kr, sub, ks, lane), qf[ks], sa, 0, 0, 0);
           pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(vr, sub, ks, lane), df[ks], pa, 0, 0, 0);
         }
+        // P at its bfloat16 storage precision (the value dV = P^T dO uses),
+        // dS = P (dP - D) / sqrt(dh); masked entries (diagonal and tail
+        // steps only): exp2(-inf) = 0
         float ds[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = k0 + 32 * sub + acc_key(r, h);
-          // masked entries: exp2(-inf) = 0 (a select, no branch); P at its
-          // bfloat16 storage precision (the value dV = P^T dO uses)
-          const float a = fmaf(sa[r], c2, -ls);
-          const float arg = (!edge | ((key <= q) & (key < T))) ? a : -INFINITY;
-          const float p = bf2f(f2bf(__builtin_amdgcn_exp2f(arg)));
-          ds[r] = scale * p * (pa[r] - D);
+        for (int r = 0; r < 16; r += 2) {
+          float a0 = fmaf(sa[r], c2, -ls), a1 = fmaf(sa[r + 1], c2, -ls);
+          if (edge) {
+            const int key = k0 + 32 * sub + acc_key(r, h);  // key of r + 1 is key + 1
+            a0 = ((key <= q) & (key < T)) ? a0 : -INFINITY;
+            a1 = ((key + 1 <= q) & (key + 1 < T)) ? a1 : -INFINITY;
+          }
+          const uint32_t u = pack_bf2(__builtin_amdgcn_exp2f(a0), __builtin_amdgcn_exp2f(a1));
+          ds[r] = bf_lo(u) * fmaf(pa[r], scale, -Ds);
+          ds[r + 1] = bf_hi(u) * fmaf(pa[r + 1], scale, -Ds);
         }
         const bf16x8 d0 = pack8(ds), d1 = pack8(ds + 8);
 #pragma unroll
@@ -520,23 +532,32 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
           sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(qrow[stg], sub, ks, lane), kf[ks], sa, 0, 0, 0);
           pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(orow_t[stg], sub, ks, lane), vf[ks], pa, 0, 0, 0);
         }
-        float p[16], ds[16];
+        // P in bfloat16 (packed pairs: directly the dV operand), dS = P (dP - D)
+        // / sqrt(dh); masked entries (diagonal and tail steps only): 0
+        uint32_t pu[8];
+        float ds[16];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int qi = 32 * sub + 8 * g + 4 * h;  // query of registers 4g..4g+3, within the step
           const f32x4 lv = *reinterpret_cast<const f32x4*>(&lsd[stg][0][qi]);
           const f32x4 dv = *reinterpret_cast<const f32x4*>(&lsd[stg][1][qi]);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
+          for (int e = 0; e < 4; e += 2) {
             const int r = 4 * g + e, qq = qs + qi + e;
-            const float a = fmaf(sa[r], c2, -lv[e]);
-            const float arg = (!edge | ((qq >= key) & (qq < T))) ? a : -INFINITY;  // masked: exp2 -> 0
-            const float pe = bf2f(f2bf(__builtin_amdgcn_exp2f(arg)));
-            p[r] = pe;
-            ds[r] = scale * pe * (pa[r] - dv[e]);
+            float a0 = fmaf(sa[r], c2, -lv[e]), a1 = fmaf(sa[r + 1], c2, -lv[e + 1]);
+            if (edge) {
+              a0 = ((qq >= key) & (qq < T)) ? a0 : -INFINITY;
+              a1 = ((qq + 1 >= key) & (qq + 1 < T)) ? a1 : -INFINITY;
+            }
+            const uint32_t u = pack_bf2(__builtin_amdgcn_exp2f(a0), __builtin_amdgcn_exp2f(a1));
+            pu[r >> 1] = u;
+            ds[r] = bf_lo(u) * fmaf(pa[r], scale, -dv[e] * scale);
+            ds[r + 1] = bf_hi(u) * fmaf(pa[r + 1], scale, -dv[e + 1] * scale);
           }
         }
-        const bf16x8 p0 = pack8(p), p1 = pack8(p + 8), d0 = pack8(ds), d1 = pack8(ds + 8);
+        const bf16x8 p0 = __builtin_bit_cast(bf16x8, u32x4{pu[0], pu[1], pu[2], pu[3]});
+        const bf16x8 p1 = __builtin_bit_cast(bf16x8, u32x4{pu[4], pu[5], pu[6], pu[7]});
+        const bf16x8 d0 = pack8(ds), d1 = pack8(ds + 8);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
           vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[stg], db * 32, 2 * sub, lane), p0, vacc[db], 0, 0, 0);
