@@ -197,10 +197,12 @@ struct layup_ctx {
   //   dqb: dQ, dK, dV (qkv projection)
   bf16_t *dyA[2] = {nullptr, nullptr}, *dfb[2] = {nullptr, nullptr};
   bf16_t *dyB[2] = {nullptr, nullptr}, *dqb[2] = {nullptr, nullptr};
-  // ev_wr[k][p]: operand k of parity p written (compute stream);
-  // ev_rd[k][p]: its dW GEMM and bias sum done (update stream);
+  // ev_mid[p]: the first half of block parity p's operands written (dfb, dyB;
+  // compute stream) -- the others (dyA, dqb) are covered by the unit events;
+  // ev_rd[k][p]: operand k's dW GEMM and bias sum done (update stream);
   // ev_dx: a dX GEMM issued (fused schedule: dW runs after it)
-  hipEvent_t ev_wr[4][2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
+  hipEvent_t ev_mid[2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
+  bool unit_recorded = false;  // the backward recorded its unit event itself
   float *ln_part = nullptr, *cs_part = nullptr;
   int64_t cs_part_floats = 0;
   ColsumScratch cs() const { return ColsumScratch{cs_part, cs_part_floats}; }
@@ -491,8 +493,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     HIPCHK(c, launch_layernorm_bwd(c->da, c->xL, c->meanf, c->rstdf, fl.p("lnf.g"), nullptr,
                                    c->dx[0], c->dyA[q], c->ln_part, fl.g("lnf.g"), fl.g("lnf.b"), N,
                                    (int)d, s), "lnf backward");
-    HIPCHK(c, rec(c->ev_wr[OP_A][q], s), "record operand written");
-    return LAYUP_OK;
+    return LAYUP_OK;  // the unit event orders dyA for the update stream
   }
   if (u == 0) {
     HIPCHK(c, launch_embed_bwd(c->dx[c->cur_dx], (const int32_t*)c->sorted, fl.g("wte"), fl.g("wpe"),
@@ -514,7 +515,6 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   // A operand is dY^T, whose row sums it accumulates from the fragments.
   auto weight_grads = [&](int op, Gemm dw, const std::string& wname, const char* bname,
                           const char* what) -> layup_status {
-    HIPCHK(c, wait(sw, c->ev_wr[op][pq]), "wait operand written");
     if (fz) {
       HIPCHK(c, rec(c->ev_dx, s), "record dX issued");
       HIPCHK(c, wait(sw, c->ev_dx), "wait dX");
@@ -529,19 +529,23 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   dg.aux = A.f;
   HIPCHK(c, wait(s, c->ev_rd[OP_F][pq]), "wait operand free");
   TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
-  HIPCHK(c, rec(c->ev_wr[OP_F][pq], s), "record operand written");
+  // dyA was written before the previous unit event, which the update stream
+  // has waited for
   TRY(weight_grads(OP_A, mk(false, false, d, F, N, dyA, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
                    p + "mproj.w", "mproj.b", "mproj dW + db"));
   // MLP input projection: dY = df16
   Gemm fcx = mk(true, false, N, d, F, df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
   TRY(run_gemm(c, fcx, s, "fc dX", true));
-  TRY(weight_grads(OP_F, mk(false, false, F, d, N, df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
-                   p + "fc.w", "fc.b", "fc dW + db"));
   HIPCHK(c, wait(s, c->ev_rd[OP_B][pq]), "wait operand free");
   HIPCHK(c, launch_layernorm_bwd(c->da, A.h, A.mean2, A.rstd2, fl.p(p + "ln2.g"), dxo, c->dh,
                                  dyB, c->ln_part, fl.g(p + "ln2.g"), fl.g(p + "ln2.b"), N, (int)d,
                                  s), "ln2 backward");
-  HIPCHK(c, rec(c->ev_wr[OP_B][pq], s), "record operand written");
+  // one event for df16 and dyB (each event record on the compute stream
+  // costs a few microseconds of idle time there)
+  HIPCHK(c, rec(c->ev_mid[pq], s), "record operands written");
+  HIPCHK(c, wait(sw, c->ev_mid[pq]), "wait operands written");
+  TRY(weight_grads(OP_F, mk(false, false, F, d, N, df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
+                   p + "fc.w", "fc.b", "fc dW + db"));
   // attention output projection: dY = dyB = bf16(dh) from the LayerNorm backward above
   Gemm prx = mk(true, false, N, d, d, dyB, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
   TRY(run_gemm(c, prx, s, "proj dX", true));
@@ -583,12 +587,9 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     TRY(run_gemm(c, batched(mk(false, false, T, dh, T, c->dS, T, A.qkv, 3 * d, dq16 + d, 3 * d,
                                EPI_BF16), H * TT, TT, T * 3 * d, dh, T * 3 * d, dh, CAUSAL_A_UPPER), s, "dK"));
   }
-  HIPCHK(c, rec(c->ev_wr[OP_Q][pq], s), "record operand written");
   // qkv projection: dY = dq16
   Gemm qx = mk(true, false, N, d, 3 * d, dq16, 3 * d, fl.w16(p + "qkv.w"), d, c->da, d, EPI_F32);
   TRY(run_gemm(c, qx, s, "qkv dX", true));
-  TRY(weight_grads(OP_Q, mk(false, false, 3 * d, d, N, dq16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d, EPI_F32),
-                   p + "qkv.w", "qkv.b", "qkv dW + db"));
   // LayerNorm 1; its bf16 dx is the next block's output-gradient operand
   const int nq = pq ^ 1;
   if (l > 0) HIPCHK(c, wait(s, c->ev_rd[OP_A][nq]), "wait operand free");
@@ -596,7 +597,16 @@ layup_status gpt_backward(layup_ctx* c, int u) {
                                  l > 0 ? c->dyA[nq] : nullptr, c->ln_part, fl.g(p + "ln1.g"),
                                  fl.g(p + "ln1.b"), N, (int)d,
                                  s), "ln1 backward");
-  if (l > 0) HIPCHK(c, rec(c->ev_wr[OP_A][nq], s), "record operand written");
+  if (side) {
+    // the unit event (compute stream's part of the unit done) also orders
+    // dq16 and the next block's dyA for the update stream; the qkv dW GEMM
+    // follows it there, ahead of the unit's update
+    HIPCHK(c, hipEventRecord(c->ev_unit[u], s), "record unit event");
+    HIPCHK(c, hipStreamWaitEvent(sw, c->ev_unit[u], 0), "wait unit event");
+    c->unit_recorded = true;
+  }
+  TRY(weight_grads(OP_Q, mk(false, false, 3 * d, d, N, dq16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d, EPI_F32),
+                   p + "qkv.w", "qkv.b", "qkv dW + db"));
   c->cur_dx ^= 1;
   return LAYUP_OK;
 }
@@ -849,10 +859,11 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
   }
   // ordering events between the compute stream and the update stream's dW work
   bool ev_ok = hipEventCreateWithFlags(&c->ev_dx, hipEventDisableTiming) == hipSuccess;
-  for (int k = 0; k < 4; ++k)
-    for (int q = 0; q < 2; ++q)
-      ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_wr[k][q], hipEventDisableTiming) == hipSuccess &&
-              hipEventCreateWithFlags(&c->ev_rd[k][q], hipEventDisableTiming) == hipSuccess;
+  for (int q = 0; q < 2; ++q) {
+    ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_mid[q], hipEventDisableTiming) == hipSuccess;
+    for (int k = 0; k < 4; ++k)
+      ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_rd[k][q], hipEventDisableTiming) == hipSuccess;
+  }
   if (!ev_ok) {
     layup_destroy(c);
     return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
@@ -871,9 +882,8 @@ void layup_destroy(layup_ctx* ctx) {
   if (ctx->ev_start) hipEventDestroy(ctx->ev_start);
   if (ctx->ev_fwd_end) hipEventDestroy(ctx->ev_fwd_end);
   if (ctx->ev_join) hipEventDestroy(ctx->ev_join);
-  for (auto& row : ctx->ev_wr)
-    for (auto e : row)
-      if (e) hipEventDestroy(e);
+  for (auto e : ctx->ev_mid)
+    if (e) hipEventDestroy(e);
   for (auto& row : ctx->ev_rd)
     for (auto e : row)
       if (e) hipEventDestroy(e);
@@ -923,9 +933,10 @@ layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit) {
   if (unit != ctx->next_backward)
     return fail(ctx, LAYUP_ERR_STATE, "units must be backpropagated in reverse order, expected " +
                                           std::to_string(ctx->next_backward));
+  ctx->unit_recorded = false;
   layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_backward(ctx, unit) : mlp_backward(ctx, unit);
   if (st != LAYUP_OK) return st;
-  HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->sc), "record unit event");
+  if (!ctx->unit_recorded) HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->sc), "record unit event");
   if (ctx->dw_side()) {
     // the unit's gradients are complete once both streams' parts are: the
     // event is re-recorded on the update stream behind the compute stream's
