@@ -203,6 +203,7 @@ struct layup_ctx {
   // ev_dx: a dX GEMM issued (fused schedule: dW runs after it)
   hipEvent_t ev_mid[2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
   hipEvent_t ev_head = nullptr;  // the head's dW done (update stream)
+  hipEvent_t ev_sort = nullptr;  // the token sort done (update stream)
   bool unit_recorded = false;  // the backward recorded its unit event itself
   float *ln_part = nullptr, *cs_part = nullptr;
   int64_t cs_part_floats = 0;
@@ -401,8 +402,16 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
   Flat fl{c};
   HIPCHK(c, launch_embed_fwd(tokens, fl.p("wte"), fl.p("wpe"), c->acts[0].x, (int)B, (int)T, (int)d,
                              g.vocab, s), "embedding");
+  // the token positions sorted by token (for the embedding backward at the
+  // end of the step): with a separate update stream the sort runs there,
+  // off the forward's critical path, after everything the compute stream
+  // had done when the step started (the previous step's embedding backward
+  // read the sorted list)
+  const hipStream_t ss = c->dw_side() ? c->su : s;
+  if (c->dw_side()) HIPCHK(c, hipStreamWaitEvent(ss, c->ev_start, 0), "wait step start");
   HIPCHK(c, launch_token_sort(tokens, (int)B, (int)T, g.vocab, nullptr, (int32_t*)c->sorted, nullptr,
-                              nullptr, nullptr, s), "token sort");
+                              nullptr, nullptr, ss), "token sort");
+  if (c->dw_side()) HIPCHK(c, hipEventRecord(c->ev_sort, ss), "record token sort");
   for (int l = 0; l < g.n_layer; ++l) {
     BlockActs& A = c->acts[l];
     const std::string p = "h" + std::to_string(l) + ".";
@@ -505,6 +514,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   }
   if (u == 0) {
     HIPCHK(c, wait(s, c->ev_head), "wait head dW");  // the embedding adds into the wte gradient
+    HIPCHK(c, wait(s, c->ev_sort), "wait token sort");
     HIPCHK(c, launch_embed_bwd(c->dx[c->cur_dx], (const int32_t*)c->sorted, fl.g("wte"), fl.g("wpe"),
                                (int)B, (int)T, (int)d, g.vocab, s), "embedding backward");
     return LAYUP_OK;
@@ -872,7 +882,8 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
   }
   // ordering events between the compute stream and the update stream's dW work
   bool ev_ok = hipEventCreateWithFlags(&c->ev_dx, hipEventDisableTiming) == hipSuccess;
-  ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_head, hipEventDisableTiming) == hipSuccess;
+  ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_head, hipEventDisableTiming) == hipSuccess &&
+          hipEventCreateWithFlags(&c->ev_sort, hipEventDisableTiming) == hipSuccess;
   for (int q = 0; q < 2; ++q) {
     ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_mid[q], hipEventDisableTiming) == hipSuccess;
     for (int k = 0; k < 4; ++k)
@@ -903,6 +914,7 @@ void layup_destroy(layup_ctx* ctx) {
       if (e) hipEventDestroy(e);
   if (ctx->ev_dx) hipEventDestroy(ctx->ev_dx);
   if (ctx->ev_head) hipEventDestroy(ctx->ev_head);
+  if (ctx->ev_sort) hipEventDestroy(ctx->ev_sort);
   delete ctx;
 }
 
