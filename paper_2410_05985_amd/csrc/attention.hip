@@ -85,7 +85,9 @@ __device__ __forceinline__ void fetch(Stage<DH, ROWS>& st, const bf16_t* m, int6
 #pragma unroll
   for (int i = 0; i < Stage<DH, ROWS>::PER; ++i) {
     const int idx = threadIdx.x + AT_THREADS * i;
-    if (idx < Stage<DH, ROWS>::CHUNKS) {
+    // the guard is compiled out when the chunks fill every thread's slots
+    // (branch-free loads keep the compiler's wait counts exact)
+    if (Stage<DH, ROWS>::CHUNKS % AT_THREADS == 0 || idx < Stage<DH, ROWS>::CHUNKS) {
       const int r = idx / Stage<DH, ROWS>::LPR, c = idx % Stage<DH, ROWS>::LPR;
       st.v[i] = *reinterpret_cast<const u32x4*>(m + (int64_t)min(r0 + r, T - 1) * ld + 8 * c);
     }
@@ -97,7 +99,7 @@ __device__ __forceinline__ void put(const Stage<DH, ROWS>& st, char* lds) {
 #pragma unroll
   for (int i = 0; i < Stage<DH, ROWS>::PER; ++i) {
     const int idx = threadIdx.x + AT_THREADS * i;
-    if (idx < Stage<DH, ROWS>::CHUNKS) {
+    if (Stage<DH, ROWS>::CHUNKS % AT_THREADS == 0 || idx < Stage<DH, ROWS>::CHUNKS) {
       const int r = idx / Stage<DH, ROWS>::LPR, c = idx % Stage<DH, ROWS>::LPR;
       *reinterpret_cast<u32x4*>(lds + (TR ? tr_off<DH>(r, c) : row_off<DH>(r, c))) = st.v[i];
     }
@@ -158,6 +160,11 @@ __device__ __forceinline__ bf16x8 pack8(const float* v) {
   w[3] = pack_bf2(v[6], v[7]);
   return __builtin_bit_cast(bf16x8, w);
 }
+
+template <int V>
+struct AtC {
+  static constexpr int value = V;
+};
 
 // The two bfloat16 halves of a packed pair, as floats.
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __builtin_bit_cast(float, u << 16); }
@@ -466,7 +473,7 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
   __shared__ __attribute__((aligned(1024))) char qtr[2][TB];
   __shared__ __attribute__((aligned(1024))) char orow_t[2][TB];
   __shared__ __attribute__((aligned(1024))) char otr[2][TB];
-  __shared__ __attribute__((aligned(16))) float lsd[2][2][AT_STEP];  // [stage][lse, D][query]
+  __shared__ __attribute__((aligned(16))) float lsd[2][2][AT_STEP];  // [stage][lse, D/sqrt(dh)][query]
   KItem it;
   if (!k_item(T, B, H, it)) return;
   const int lane = threadIdx.x & 63;
@@ -492,33 +499,39 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
   for (int i = 0; i < DB; ++i)
 #pragma unroll
     for (int r = 0; r < 16; ++r) kacc[i][r] = vacc[i][r] = 0.f;
-  Stage<DH, AT_STEP> sq, so;
-  float sl = 0.f;  // one lse or D value per thread of the first 128
-  auto fetch_l = [&](int q0) {
-    const int t = threadIdx.x;
-    if (t < 2 * AT_STEP) sl = (t < AT_STEP ? lsep : Dp)[min(q0 + (t % AT_STEP), T - 1)];
+  // Q and dO tiles (and the lse and D values) of a query step are loaded into
+  // registers two steps ahead (slots by step parity, as the LDS stages), so a
+  // load has two steps' compute to land before its stores into LDS.
+  Stage<DH, AT_STEP> sq[2], so[2];
+  float sl[2] = {0.f, 0.f};  // one lse or D value per thread of the first 128
+  auto fetch_step = [&](auto S, int st) {
+    constexpr int k = decltype(S)::value;
+    fetch<DH, AT_STEP>(sq[k], Qp, ld, st * AT_STEP, T);
+    fetch<DH, AT_STEP>(so[k], dOp, d, st * AT_STEP, T);
+    const int t = threadIdx.x & (2 * AT_STEP - 1);  // every thread loads (one wait count for all)
+    sl[k] = (t < AT_STEP ? lsep : Dp)[min(st * AT_STEP + (t % AT_STEP), T - 1)];
   };
-  auto put_l = [&](int stg) {
+  auto put_step = [&](auto S) {
+    constexpr int k = decltype(S)::value;
+    put<DH, AT_STEP, false>(sq[k], qrow[k]);
+    put<DH, AT_STEP, true>(sq[k], qtr[k]);
+    put<DH, AT_STEP, false>(so[k], orow_t[k]);
+    put<DH, AT_STEP, true>(so[k], otr[k]);
     const int t = threadIdx.x;
-    if (t < 2 * AT_STEP) lsd[stg][t / AT_STEP][t % AT_STEP] = sl;
+    if (t < 2 * AT_STEP) lsd[k][t / AT_STEP][t % AT_STEP] = t < AT_STEP ? sl[k] : sl[k] * scale;
   };
-  const int q0 = it.first * AT_STEP;
-  fetch<DH, AT_STEP>(sq, Qp, ld, q0, T);
-  fetch<DH, AT_STEP>(so, dOp, d, q0, T);
-  fetch_l(q0);
-  put<DH, AT_STEP, false>(sq, qrow[0]);
-  put<DH, AT_STEP, true>(sq, qtr[0]);
-  put<DH, AT_STEP, false>(so, orow_t[0]);
-  put<DH, AT_STEP, true>(so, otr[0]);
-  put_l(0);
+  fetch_step(AtC<0>{}, it.first);
+  put_step(AtC<0>{});
+  if (it.first + 1 < it.nst) fetch_step(AtC<1>{}, it.first + 1);
   loop_entry_barrier();
-  for (int st = it.first; st < it.nst; ++st) {
-    const int stg = (st - it.first) & 1;
-    if (st + 1 < it.nst) {
-      fetch<DH, AT_STEP>(sq, Qp, ld, (st + 1) * AT_STEP, T);
-      fetch<DH, AT_STEP>(so, dOp, d, (st + 1) * AT_STEP, T);
-      fetch_l((st + 1) * AT_STEP);
-    }
+  // step st: its tiles in LDS stage P = (st - first) % 2, the next step's in
+  // register slot P ^ 1; slot P is free for step st + 2
+  auto step = [&](auto PC, int st) {
+    constexpr int P = decltype(PC)::value;
+    // issued on every step (a step past the end reloads the last one, never
+    // stored) so that the wait before the stores below counts the same
+    // loads on every path
+    fetch_step(AtC<P>{}, min(st + 2, it.nst - 1));
     if (it.active && st >= it.mine) {
       const int qs = st * AT_STEP;
       const bool edge = qs < it.kb * 32 + 32 || qs + AT_STEP > T;
@@ -529,8 +542,8 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
         for (int r = 0; r < 16; ++r) sa[r] = pa[r] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(qrow[stg], sub, ks, lane), kf[ks], sa, 0, 0, 0);
-          pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(orow_t[stg], sub, ks, lane), vf[ks], pa, 0, 0, 0);
+          sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(qrow[P], sub, ks, lane), kf[ks], sa, 0, 0, 0);
+          pa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_frag<DH>(orow_t[P], sub, ks, lane), vf[ks], pa, 0, 0, 0);
         }
         // P in bfloat16 (packed pairs: directly the dV operand), dS = P (dP - D)
         // / sqrt(dh); masked entries (diagonal and tail steps only): 0
@@ -539,8 +552,8 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int qi = 32 * sub + 8 * g + 4 * h;  // query of registers 4g..4g+3, within the step
-          const f32x4 lv = *reinterpret_cast<const f32x4*>(&lsd[stg][0][qi]);
-          const f32x4 dv = *reinterpret_cast<const f32x4*>(&lsd[stg][1][qi]);
+          const f32x4 lv = *reinterpret_cast<const f32x4*>(&lsd[P][0][qi]);
+          const f32x4 dv = *reinterpret_cast<const f32x4*>(&lsd[P][1][qi]);
 #pragma unroll
           for (int e = 0; e < 4; e += 2) {
             const int r = 4 * g + e, qq = qs + qi + e;
@@ -551,8 +564,8 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
             }
             const uint32_t u = pack_bf2(__builtin_amdgcn_exp2f(a0), __builtin_amdgcn_exp2f(a1));
             pu[r >> 1] = u;
-            ds[r] = bf_lo(u) * fmaf(pa[r], scale, -dv[e] * scale);
-            ds[r + 1] = bf_hi(u) * fmaf(pa[r + 1], scale, -dv[e + 1] * scale);
+            ds[r] = bf_lo(u) * fmaf(pa[r], scale, -dv[e]);
+            ds[r + 1] = bf_hi(u) * fmaf(pa[r + 1], scale, -dv[e + 1]);
           }
         }
         const bf16x8 p0 = __builtin_bit_cast(bf16x8, u32x4{pu[0], pu[1], pu[2], pu[3]});
@@ -560,21 +573,19 @@ __global__ __launch_bounds__(AT_THREADS, AT_OCC_DKV(DH)) void attn_bwd_dkv_kerne
         const bf16x8 d0 = pack8(ds), d1 = pack8(ds + 8);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[stg], db * 32, 2 * sub, lane), p0, vacc[db], 0, 0, 0);
-          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[stg], db * 32, 2 * sub + 1, lane), p1, vacc[db], 0, 0, 0);
-          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[stg], db * 32, 2 * sub, lane), d0, kacc[db], 0, 0, 0);
-          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[stg], db * 32, 2 * sub + 1, lane), d1, kacc[db], 0, 0, 0);
+          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[P], db * 32, 2 * sub, lane), p0, vacc[db], 0, 0, 0);
+          vacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(otr[P], db * 32, 2 * sub + 1, lane), p1, vacc[db], 0, 0, 0);
+          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[P], db * 32, 2 * sub, lane), d0, kacc[db], 0, 0, 0);
+          kacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tr_frag<DH>(qtr[P], db * 32, 2 * sub + 1, lane), d1, kacc[db], 0, 0, 0);
         }
       }
     }
-    if (st + 1 < it.nst) {
-      put<DH, AT_STEP, false>(sq, qrow[stg ^ 1]);
-      put<DH, AT_STEP, true>(sq, qtr[stg ^ 1]);
-      put<DH, AT_STEP, false>(so, orow_t[stg ^ 1]);
-      put<DH, AT_STEP, true>(so, otr[stg ^ 1]);
-      put_l(stg ^ 1);
-    }
+    if (st + 1 < it.nst) put_step(AtC<P ^ 1>{});
     tile_barrier();
+  };
+  for (int st = it.first; st < it.nst; st += 2) {
+    step(AtC<0>{}, st);
+    if (st + 1 < it.nst) step(AtC<1>{}, st + 1);
   }
   if (!it.active || key >= T) return;
   bf16_t* rowp = dqkv + ((int64_t)it.b * T + key) * ld + it.hh * DH;
