@@ -546,7 +546,7 @@ def bench_kernels(args, torch, LU, S):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU: the layer-wise step of one worker; "
+        print(json.dumps({"error": "the benchmark runs on one GPU: the layer-wise step of one worker; "
                                    "multi-GPU runs are not part of it", "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
