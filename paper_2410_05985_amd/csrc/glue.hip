@@ -828,19 +828,25 @@ __global__ __launch_bounds__(CE_T) void ce_regs_kernel(const bf16_t* z, int64_t 
 
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B, int T,
                              int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
-                             hipStream_t s) {
+                             hipStream_t s, int64_t mean_rows) {
   if (ld % 8 || ld < V) return hipErrorInvalidValue;
   const int64_t rows = (int64_t)B * T;
+  const int64_t mr = mean_rows > 0 ? mean_rows : rows;  // rows of the mean the gradient is of
   const int64_t nv = ld / 8;
   if (nv <= CE_T * 4)
-    ce_regs_kernel<4><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+    ce_regs_kernel<4><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, mr, dlogits, loss_rows);
   else if (nv <= CE_T * 13)  // GPT-2's 50304-column logits
-    ce_regs_kernel<13><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+    ce_regs_kernel<13><<<(unsigned)rows, CE_T, 0, s>>>(logits, ld, tokens, T, V, mr, dlogits, loss_rows);
   else
-    ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, rows, dlogits, loss_rows);
+    ce_kernel<<<(unsigned)rows, 256, 0, s>>>(logits, ld, tokens, T, V, mr, dlogits, loss_rows);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !loss_out) return e;
   mean_kernel<<<1, 1024, 0, s>>>(loss_rows, rows, loss_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_row_mean(const float* x, int64_t n, float* out, hipStream_t s) {
+  mean_kernel<<<1, 1024, 0, s>>>(x, n, out);
   return hipGetLastError();
 }
 

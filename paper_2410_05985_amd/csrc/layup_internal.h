@@ -193,9 +193,15 @@ hipError_t launch_attention_fwd(const bf16_t* qkv, float* lse, bf16_t* O, float*
 hipError_t launch_attention_bwd(const bf16_t* qkv, const float* lse, const bf16_t* dO, const float* Of,
                                 float* D, bf16_t* dqkv, int B, int H, int T, int dh, float scale,
                                 hipStream_t s);
+// Cross-entropy over rows [B*T] of logits (row r = b*T + t predicts token
+// t + 1 of sequence b) with its gradient written to dlogits (may alias the
+// logits); the gradient is of the mean over mean_rows rows (0: the B*T rows
+// of this call, so a batch can be taken in parts); loss_out, when given,
+// receives the mean of this call's loss rows.
 hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* tokens, int B,
                              int T, int V, bf16_t* dlogits, float* loss_rows, float* loss_out,
-                             hipStream_t s);
+                             hipStream_t s, int64_t mean_rows = 0);
+hipError_t launch_row_mean(const float* x, int64_t n, float* out, hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s);
 hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
                               const ColsumScratch& cs, float* out, hipStream_t s);

@@ -204,6 +204,7 @@ struct layup_ctx {
   hipEvent_t ev_mid[2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
   hipEvent_t ev_head = nullptr;  // the head's dW done (update stream)
   hipEvent_t ev_sort = nullptr;  // the token sort done (update stream)
+  hipEvent_t ev_fwd_half = nullptr;  // the forward's second half done (update stream)
   bool unit_recorded = false;  // the backward recorded its unit event itself
   float *ln_part = nullptr, *cs_part = nullptr;
   int64_t cs_part_floats = 0;
@@ -400,76 +401,99 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
                 dh = d / H, Vp = align64(g.vocab);
   const float scale = 1.0f / sqrtf((float)dh);
   Flat fl{c};
-  HIPCHK(c, launch_embed_fwd(tokens, fl.p("wte"), fl.p("wpe"), c->acts[0].x, (int)B, (int)T, (int)d,
-                             g.vocab, s), "embedding");
-  // the token positions sorted by token (for the embedding backward at the
-  // end of the step): with a separate update stream the sort runs there,
-  // off the forward's critical path, after everything the compute stream
-  // had done when the step started (the previous step's embedding backward
-  // read the sorted list)
-  const hipStream_t ss = c->dw_side() ? c->su : s;
-  if (c->dw_side()) HIPCHK(c, hipStreamWaitEvent(ss, c->ev_start, 0), "wait step start");
-  HIPCHK(c, launch_token_sort(tokens, (int)B, (int)T, g.vocab, nullptr, (int32_t*)c->sorted, nullptr,
-                              nullptr, nullptr, ss), "token sort");
-  if (c->dw_side()) HIPCHK(c, hipEventRecord(c->ev_sort, ss), "record token sort");
-  for (int l = 0; l < g.n_layer; ++l) {
-    BlockActs& A = c->acts[l];
-    const std::string p = "h" + std::to_string(l) + ".";
-    float* x_next = (l + 1 < g.n_layer) ? c->acts[l + 1].x : c->xL;
-    HIPCHK(c, launch_layernorm_fwd(A.x, fl.p(p + "ln1.g"), fl.p(p + "ln1.b"), A.a, A.mean1, A.rstd1,
-                                   N, (int)d, s), "ln1");
-    Gemm q = mk(true, true, N, 3 * d, d, A.a, d, fl.w16(p + "qkv.w"), d, A.qkv, 3 * d, EPI_BF16);
-    q.bias = fl.p(p + "qkv.b");
-    TRY(run_gemm(c, q, s, "qkv forward"));
-    if (A.of) {
-      HIPCHK(c, launch_attention_fwd(A.qkv, A.lse, A.o, A.of, (int)B, (int)H, (int)T, (int)dh, scale, s),
-             "attention");
-    } else {
-    // scores S[z] = Q_h K_h^T, z = b*H + h
-    Gemm sg = mk(true, true, T, T, dh, A.qkv, 3 * d, A.qkv + d, 3 * d, c->S, T, EPI_F32);
-    sg.batch = (int)(B * H);
-    sg.inner = (int)H;
-    sg.a_outer = sg.b_outer = T * 3 * d;
-    sg.a_inner = sg.b_inner = dh;
-    sg.c_outer = H * T * T;
-    sg.c_inner = T * T;
-    sg.causal = CAUSAL_OUT_LOWER;
-    TRY(run_gemm(c, sg, s, "scores"));
-    HIPCHK(c, launch_softmax_fwd(c->S, A.P, B * H, (int)T, scale, s), "softmax");
-    // o_h = P V_h
-    Gemm pv = mk(true, false, T, dh, T, A.P, T, A.qkv + 2 * d, 3 * d, A.o, d, EPI_BF16);
-    pv.batch = (int)(B * H);
-    pv.inner = (int)H;
-    pv.a_outer = H * T * T;
-    pv.a_inner = T * T;
-    pv.b_outer = T * 3 * d;
-    pv.b_inner = dh;
-    pv.c_outer = T * d;
-    pv.c_inner = dh;
-    pv.causal = CAUSAL_A_LOWER;
-    TRY(run_gemm(c, pv, s, "attention output"));
+  // The forward of sequences [b0, b0 + nb) on stream st.  With an update
+  // stream (idle during the forward) the batch is taken in two halves, the
+  // second there; every row's arithmetic is the same either way.
+  auto part = [&](int64_t b0, int64_t nb, hipStream_t st) -> layup_status {
+    const int64_t r0 = b0 * T, n = nb * T;
+    const int32_t* tk = tokens + b0 * (T + 1);
+    HIPCHK(c, launch_embed_fwd(tk, fl.p("wte"), fl.p("wpe"), c->acts[0].x + r0 * d, (int)nb, (int)T, (int)d,
+                               g.vocab, st), "embedding");
+    for (int l = 0; l < g.n_layer; ++l) {
+      BlockActs& A = c->acts[l];
+      const std::string p = "h" + std::to_string(l) + ".";
+      float* x_next = ((l + 1 < g.n_layer) ? c->acts[l + 1].x : c->xL) + r0 * d;
+      bf16_t* qkv = A.qkv + r0 * 3 * d;
+      bf16_t* o = A.o + r0 * d;
+      HIPCHK(c, launch_layernorm_fwd(A.x + r0 * d, fl.p(p + "ln1.g"), fl.p(p + "ln1.b"), A.a + r0 * d,
+                                     A.mean1 + r0, A.rstd1 + r0, n, (int)d, st), "ln1");
+      Gemm q = mk(true, true, n, 3 * d, d, A.a + r0 * d, d, fl.w16(p + "qkv.w"), d, qkv, 3 * d, EPI_BF16);
+      q.bias = fl.p(p + "qkv.b");
+      TRY(run_gemm(c, q, st, "qkv forward"));
+      if (A.of) {
+        HIPCHK(c, launch_attention_fwd(qkv, A.lse + b0 * H * T, o, A.of + r0 * d, (int)nb, (int)H, (int)T,
+                                       (int)dh, scale, st), "attention");
+      } else {
+        // scores S[z] = Q_h K_h^T, z = b*H + h
+        float* S = c->S + b0 * H * T * T;
+        bf16_t* P = A.P + b0 * H * T * T;
+        Gemm sg = mk(true, true, T, T, dh, qkv, 3 * d, qkv + d, 3 * d, S, T, EPI_F32);
+        sg.batch = (int)(nb * H);
+        sg.inner = (int)H;
+        sg.a_outer = sg.b_outer = T * 3 * d;
+        sg.a_inner = sg.b_inner = dh;
+        sg.c_outer = H * T * T;
+        sg.c_inner = T * T;
+        sg.causal = CAUSAL_OUT_LOWER;
+        TRY(run_gemm(c, sg, st, "scores"));
+        HIPCHK(c, launch_softmax_fwd(S, P, nb * H, (int)T, scale, st), "softmax");
+        // o_h = P V_h
+        Gemm pv = mk(true, false, T, dh, T, P, T, qkv + 2 * d, 3 * d, o, d, EPI_BF16);
+        pv.batch = (int)(nb * H);
+        pv.inner = (int)H;
+        pv.a_outer = H * T * T;
+        pv.a_inner = T * T;
+        pv.b_outer = T * 3 * d;
+        pv.b_inner = dh;
+        pv.c_outer = T * d;
+        pv.c_inner = dh;
+        pv.causal = CAUSAL_A_LOWER;
+        TRY(run_gemm(c, pv, st, "attention output"));
+      }
+      Gemm pr = mk(true, true, n, d, d, o, d, fl.w16(p + "proj.w"), d, A.h + r0 * d, d, EPI_F32);
+      pr.bias = fl.p(p + "proj.b");
+      pr.aux = A.x + r0 * d;
+      TRY(run_gemm(c, pr, st, "proj forward"));
+      HIPCHK(c, launch_layernorm_fwd(A.h + r0 * d, fl.p(p + "ln2.g"), fl.p(p + "ln2.b"), A.a2 + r0 * d,
+                                     A.mean2 + r0, A.rstd2 + r0, n, (int)d, st), "ln2");
+      Gemm fc = mk(true, true, n, F, d, A.a2 + r0 * d, d, fl.w16(p + "fc.w"), d, A.f + r0 * F, F, EPI_GELU);
+      fc.bias = fl.p(p + "fc.b");
+      fc.C2 = A.gl + r0 * F;
+      TRY(run_gemm(c, fc, st, "fc forward"));
+      Gemm mp = mk(true, true, n, d, F, A.gl + r0 * F, F, fl.w16(p + "mproj.w"), F, x_next, d, EPI_F32);
+      mp.bias = fl.p(p + "mproj.b");
+      mp.aux = A.h + r0 * d;
+      TRY(run_gemm(c, mp, st, "mproj forward"));
     }
-    Gemm pr = mk(true, true, N, d, d, A.o, d, fl.w16(p + "proj.w"), d, A.h, d, EPI_F32);
-    pr.bias = fl.p(p + "proj.b");
-    pr.aux = A.x;
-    TRY(run_gemm(c, pr, s, "proj forward"));
-    HIPCHK(c, launch_layernorm_fwd(A.h, fl.p(p + "ln2.g"), fl.p(p + "ln2.b"), A.a2, A.mean2, A.rstd2,
-                                   N, (int)d, s), "ln2");
-    Gemm fc = mk(true, true, N, F, d, A.a2, d, fl.w16(p + "fc.w"), d, A.f, F, EPI_GELU);
-    fc.bias = fl.p(p + "fc.b");
-    fc.C2 = A.gl;
-    TRY(run_gemm(c, fc, s, "fc forward"));
-    Gemm mp = mk(true, true, N, d, F, A.gl, F, fl.w16(p + "mproj.w"), F, x_next, d, EPI_F32);
-    mp.bias = fl.p(p + "mproj.b");
-    mp.aux = A.h;
-    TRY(run_gemm(c, mp, s, "mproj forward"));
+    HIPCHK(c, launch_layernorm_fwd(c->xL + r0 * d, fl.p("lnf.g"), fl.p("lnf.b"), c->xf + r0 * d, c->meanf + r0,
+                                   c->rstdf + r0, n, (int)d, st), "lnf");
+    Gemm hd = mk(true, true, n, Vp, d, c->xf + r0 * d, d, fl.w16("wte"), d, c->logits + r0 * Vp, Vp, EPI_BF16);
+    TRY(run_gemm(c, hd, st, "head forward"));
+    HIPCHK(c, launch_ce_fwd_bwd(c->logits + r0 * Vp, Vp, tk, (int)nb, (int)T, g.vocab, c->logits + r0 * Vp,
+                                c->loss_rows + r0, nullptr, st, N), "cross-entropy");
+    return LAYUP_OK;
+  };
+  const bool side = c->dw_side();
+  const hipStream_t s2 = side ? c->su : s;
+  // the update stream starts after everything the compute stream had done
+  // when the step started (the previous step's updates and backward)
+  if (side) HIPCHK(c, hipStreamWaitEvent(s2, c->ev_start, 0), "wait step start");
+  // one stream: the whole batch at once (half-size products are less efficient)
+  const int64_t nb0 = (side && B >= 2) ? B / 2 : B;
+  TRY(part(0, nb0, s));
+  if (nb0 < B) TRY(part(nb0, B - nb0, s2));
+  if (side) {
+    HIPCHK(c, hipEventRecord(c->ev_fwd_half, s2), "record forward half");
+    HIPCHK(c, hipStreamWaitEvent(s, c->ev_fwd_half, 0), "wait forward half");
   }
-  HIPCHK(c, launch_layernorm_fwd(c->xL, fl.p("lnf.g"), fl.p("lnf.b"), c->xf, c->meanf, c->rstdf, N,
-                                 (int)d, s), "lnf");
-  Gemm hd = mk(true, true, N, Vp, d, c->xf, d, fl.w16("wte"), d, c->logits, Vp, EPI_BF16);
-  TRY(run_gemm(c, hd, s, "head forward"));
-  HIPCHK(c, launch_ce_fwd_bwd(c->logits, Vp, tokens, (int)B, (int)T, g.vocab, c->logits, c->loss_rows,
-                              loss_out, s), "cross-entropy");
+  if (loss_out) HIPCHK(c, launch_row_mean(c->loss_rows, N, loss_out, s), "loss mean");
+  // the token positions sorted by token (for the embedding backward at the
+  // end of the step): on the update stream, off the critical path (the
+  // embedding backward waits for it); the previous step's embedding
+  // backward, which read the list, finished before the step started
+  HIPCHK(c, launch_token_sort(tokens, (int)B, (int)T, g.vocab, nullptr, (int32_t*)c->sorted, nullptr,
+                              nullptr, nullptr, s2), "token sort");
+  if (side) HIPCHK(c, hipEventRecord(c->ev_sort, s2), "record token sort");
   return LAYUP_OK;
 }
 
@@ -883,7 +907,8 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
   // ordering events between the compute stream and the update stream's dW work
   bool ev_ok = hipEventCreateWithFlags(&c->ev_dx, hipEventDisableTiming) == hipSuccess;
   ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_head, hipEventDisableTiming) == hipSuccess &&
-          hipEventCreateWithFlags(&c->ev_sort, hipEventDisableTiming) == hipSuccess;
+          hipEventCreateWithFlags(&c->ev_sort, hipEventDisableTiming) == hipSuccess &&
+          hipEventCreateWithFlags(&c->ev_fwd_half, hipEventDisableTiming) == hipSuccess;
   for (int q = 0; q < 2; ++q) {
     ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_mid[q], hipEventDisableTiming) == hipSuccess;
     for (int k = 0; k < 4; ++k)
@@ -915,6 +940,7 @@ void layup_destroy(layup_ctx* ctx) {
   if (ctx->ev_dx) hipEventDestroy(ctx->ev_dx);
   if (ctx->ev_head) hipEventDestroy(ctx->ev_head);
   if (ctx->ev_sort) hipEventDestroy(ctx->ev_sort);
+  if (ctx->ev_fwd_half) hipEventDestroy(ctx->ev_fwd_half);
   delete ctx;
 }
 
