@@ -521,11 +521,6 @@ hipError_t colsum2(const T* x, int64_t rows, int64_t cols, int64_t ld, const Col
   return hipGetLastError();
 }
 
-hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              const ColsumScratch& cs, float* out, hipStream_t s) {
-  return colsum2<bf16_t>(x, rows, cols, ld, cs, out, nullptr, 0, s);
-}
-
 hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
                              const ColsumScratch& cs, float* out, hipStream_t s) {
   return colsum2<float>(x, rows, cols, ld, cs, out, nullptr, 0, s);

@@ -203,8 +203,6 @@ hipError_t launch_ce_fwd_bwd(const bf16_t* logits, int64_t ld, const int32_t* to
                              hipStream_t s, int64_t mean_rows = 0);
 hipError_t launch_row_mean(const float* x, int64_t n, float* out, hipStream_t s);
 hipError_t launch_f32_to_bf16(const float* x, bf16_t* y, int64_t n, hipStream_t s);
-hipError_t launch_colsum_bf16(const bf16_t* x, int64_t rows, int64_t cols, int64_t ld,
-                              const ColsumScratch& cs, float* out, hipStream_t s);
 hipError_t launch_colsum_f32(const float* x, int64_t rows, int64_t cols, int64_t ld,
                              const ColsumScratch& cs, float* out, hipStream_t s);
 hipError_t launch_embed_bwd(const float* dx, const int32_t* sorted_pos, float* dwte, float* dwpe,
