@@ -625,21 +625,62 @@ __global__ __launch_bounds__(64 * WGM * WGN, OCC) void gemm_bf16_kernel(const KA
   }
 }
 
+// Sum over the splits, in split order, of the partials of four consecutive
+// columns (ne of them valid; one 128-bit load per split when vec).  The
+// loads of up to eight splits are issued before the first add, so a thread
+// waits one memory round trip per eight splits instead of one per split;
+// the additions keep the order p0 + p1 + ... of a plain loop.
+__device__ __forceinline__ f32x4 sum_partials4(const float* src, int64_t total, int splits, int ne, bool vec) {
+  f32x4 v{0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    f32x4 t[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      if (s0 + k < splits) {
+        const float* p = src + (int64_t)(s0 + k) * total;
+        if (vec) {
+          t[k] = *reinterpret_cast<const f32x4*>(p);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) t[k][e] = e < ne ? p[e] : 0.f;
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+      if (s0 + k < splits) v = s0 + k == 0 ? t[k] : v + t[k];
+  }
+  return v;
+}
+
 // Fixed-order sum of split-K partials plus the epilogue: float32 output
-// (bias, residual) or the fused weight update.  Grid: x = 1024-column chunk,
-// y = row; each thread sums four consecutive columns, with 128-bit accesses
-// when N and ldc are multiples of 4 and every pointer is 16-byte aligned.
+// (bias, residual) or the fused weight update.  One thread per four
+// consecutive columns of a row, threads numbered row-major over the M x N/4
+// groups (no idle lanes when N is not a multiple of 1024), with 128-bit
+// accesses when N and ldc are multiples of 4 and every pointer is 16-byte
+// aligned.  The thread of a row's first group also sums the row-sum partials.
 template <int EPI>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
   static_assert(EPI == EPI_F32 || EPI == EPI_UPDATE, "split-K only with the float32 or update epilogue");
-  const int64_t m = blockIdx.y;
-  const int64_t n = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
-  if (n >= P.N) return;
+  const int64_t nq = (P.N + 3) / 4;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= P.M * nq) return;
+  const int64_t m = idx / nq;
+  const int64_t n = (idx - m * nq) * 4;
+  const int ne = P.N - n < 4 ? (int)(P.N - n) : 4;
   const int64_t total = P.M * P.N;
-  if (P.rowsum && blockIdx.x == 0 && threadIdx.x == 0) {
+  if (P.rowsum && n == 0) {
     const float* rp = P.partial + P.splits * total + m;
-    float r = rp[0];
-    for (int s = 1; s < P.splits; ++s) r += rp[(int64_t)s * P.M];
+    float r = 0.f;
+    for (int s0 = 0; s0 < P.splits; s0 += 8) {
+      float t[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (s0 + k < P.splits) t[k] = rp[(int64_t)(s0 + k) * P.M];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (s0 + k < P.splits) r = s0 + k == 0 ? t[k] : r + t[k];
+    }
     P.rowsum[m] = r;
   }
   const float* src = P.partial + m * P.N + n;
@@ -648,16 +689,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
     const bool vec = ((P.N | P.ldc) & 3) == 0 && ((uintptr_t)P.partial & 15) == 0 &&
                      (((uintptr_t)P.upd.p | (uintptr_t)P.upd.m | (uintptr_t)P.upd.v | (uintptr_t)P.upd.q) & 15) == 0 &&
                      ((uintptr_t)P.upd.p16 & 7) == 0;
+    const f32x4 v = sum_partials4(src, total, P.splits, ne, vec);
     if (vec) {
-      f32x4 v = *reinterpret_cast<const f32x4*>(src);
-      for (int s = 1; s < P.splits; ++s) v += *reinterpret_cast<const f32x4*>(src + s * total);
       apply_update4(P.upd, off, v);
     } else {
-      for (int e = 0; e < 4 && n + e < P.N; ++e) {
-        float v = src[e];
-        for (int s = 1; s < P.splits; ++s) v += src[s * total + e];
-        apply_update(P.upd, off + e, v);
-      }
+      for (int e = 0; e < ne; ++e) apply_update(P.upd, off + e, v[e]);
     }
     return;
   }
@@ -665,19 +701,17 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const KArgs P) {
   const float* aux = P.aux ? reinterpret_cast<const float*>(P.aux) + m * P.ldc + n : nullptr;
   const bool vec = ((P.N | P.ldc) & 3) == 0 &&
                    (((uintptr_t)P.C | (uintptr_t)P.aux | (uintptr_t)P.bias | (uintptr_t)P.partial) & 15) == 0;
+  f32x4 v = sum_partials4(src, total, P.splits, ne, vec);
   if (vec) {
-    f32x4 v = *reinterpret_cast<const f32x4*>(src);
-    for (int s = 1; s < P.splits; ++s) v += *reinterpret_cast<const f32x4*>(src + s * total);
     if (P.bias) v += *reinterpret_cast<const f32x4*>(P.bias + n);
     if (aux) v += *reinterpret_cast<const f32x4*>(aux);
     *reinterpret_cast<f32x4*>(dst) = v;
   } else {
-    for (int e = 0; e < 4 && n + e < P.N; ++e) {
-      float v = src[e];
-      for (int s = 1; s < P.splits; ++s) v += src[s * total + e];
-      if (P.bias) v += P.bias[n + e];
-      if (aux) v += aux[e];
-      dst[e] = v;
+    for (int e = 0; e < ne; ++e) {
+      float o = v[e];
+      if (P.bias) o += P.bias[n + e];
+      if (aux) o += aux[e];
+      dst[e] = o;
     }
   }
 }
@@ -694,8 +728,9 @@ hipError_t launch_tiles(const KArgs& P, int batch, hipStream_t s) {
       gemm_bf16_kernel<BM, BN, WGM, WGN, STG, OCC, AK, BKM, EPI, true, BKV, SBS><<<grid, NT, 0, s>>>(P);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      const dim3 rgrid((unsigned)cdiv(P.N, 1024), (unsigned)P.M);
-      splitk_reduce_kernel<EPI><<<rgrid, 256, 0, s>>>(P);
+      const int64_t groups = P.M * cdiv(P.N, 4);
+      if (groups >= (1ll << 31) * 256ll) return hipErrorInvalidValue;
+      splitk_reduce_kernel<EPI><<<(unsigned)cdiv(groups, 256), 256, 0, s>>>(P);
       return hipGetLastError();
     }
   }

@@ -191,7 +191,7 @@ hipError_t launch_layernorm_fwd(const float* x, const float* g, const float* b, 
 // next-row prefetch is used while two rows fit in registers).  dg and db (column sums of dy*xh and
 // dy) are summed per wave in row order, then over the waves in wave order,
 // into one partial row per block; ln_partial_sum_kernel adds the partial rows
-// in block order.
+// in a fixed order.
 constexpr int LN_WAVES = 8;
 constexpr int LN_ROWS = 32;
 
@@ -353,27 +353,35 @@ __global__ __launch_bounds__(64 * LN_WAVES) void layernorm_bwd_kernel(
   }
 }
 
-// dg | db = the nb partial rows [nb][2d] added in row order.  A block covers
-// 64 columns (16 float4 groups) with 16 row lanes: lane l adds rows l, l+16,
-// ... in order, then the 16 lane sums are added in lane order.
-__global__ __launch_bounds__(256) void ln_partial_sum_kernel(const float* part, int64_t nb, int d,
-                                                             float* dg, float* db) {
-  __shared__ f32x4 red[16][16];
-  const int cg = threadIdx.x & 15, rl = threadIdx.x >> 4;
+// dg | db = the nb partial rows [nb][2d] summed in a fixed order.  A block
+// covers 16 columns (4 float4 groups) with 64 row lanes: lane l adds rows l,
+// l+64, ... in order (all of its loads in flight at once for nb <= 256), then
+// the 64 lane sums are added pairwise in a fixed tree (lane l += lane l+h for
+// h = 32, 16, ..., 1).  96 blocks for d = 768, so the pass is one memory
+// round trip rather than a serial walk down the partial rows.
+constexpr int LNP_COLS = 4;    // float4 column groups per block
+constexpr int LNP_LANES = 64;  // row lanes per block
+__global__ __launch_bounds__(LNP_COLS * LNP_LANES) void ln_partial_sum_kernel(const float* part, int64_t nb,
+                                                                               int d, float* dg, float* db) {
+  __shared__ f32x4 red[LNP_LANES][LNP_COLS];
+  const int cg = threadIdx.x % LNP_COLS, rl = threadIdx.x / LNP_COLS;
   const int64_t cols = 2 * (int64_t)d;
-  const int64_t c = ((int64_t)blockIdx.x * 16 + cg) * 4;
+  const int64_t c = ((int64_t)blockIdx.x * LNP_COLS + cg) * 4;
   f32x4 s{0.f, 0.f, 0.f, 0.f};
   if (c < cols) {
 #pragma unroll 4
-    for (int64_t r = rl; r < nb; r += 16) s += *reinterpret_cast<const f32x4*>(part + r * cols + c);
+    for (int64_t r = rl; r < nb; r += LNP_LANES) s += *reinterpret_cast<const f32x4*>(part + r * cols + c);
   }
   red[rl][cg] = s;
   __syncthreads();
+#pragma unroll
+  for (int h = LNP_LANES / 2; h >= 1; h >>= 1) {
+    if (rl < h) red[rl][cg] += red[rl + h][cg];
+    __syncthreads();
+  }
   if (rl == 0 && c < cols) {
-    f32x4 t = red[0][cg];
-    for (int l = 1; l < 16; ++l) t += red[l][cg];
     float* out = c < d ? dg + c : db + (c - d);
-    *reinterpret_cast<f32x4*>(out) = t;
+    *reinterpret_cast<f32x4*>(out) = red[0][cg];
   }
 }
 
@@ -403,7 +411,8 @@ hipError_t launch_layernorm_bwd(const float* dy, const float* x, const float* me
   else if (nvl == 4) e = ln_bwd_launch<4>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
   else e = ln_bwd_launch<8>(dy, x, mean, rstd, g, dres, dx, dx16, part, rows, d, nb, s);
   if (e != hipSuccess) return e;
-  ln_partial_sum_kernel<<<(unsigned)cdiv(2 * (int64_t)d, 64), 256, 0, s>>>(part, nb, d, dg, db);
+  ln_partial_sum_kernel<<<(unsigned)cdiv(2 * (int64_t)d, 4 * LNP_COLS), LNP_COLS * LNP_LANES, 0, s>>>(part, nb, d, dg,
+                                                                                                 db);
   return hipGetLastError();
 }
 

@@ -89,6 +89,17 @@ def test_gemm_long_k_split(layout):
     assert np.array_equal(a, b)
 
 
+def test_gemm_split_k_unaligned_columns():
+    """Split-K whose output rows are not a multiple of four floats (N = 130,
+    k-major B): the partial sums take the per-column path, with the bias;
+    reproducible bit for bit."""
+    a, ref = run("kk", 200, 130, 16400, bias=True, ws=True, seed=19)
+    b, _ = run("kk", 200, 130, 16400, bias=True, ws=True, seed=19)
+    compare(a, ref, 2e-2, "split-K N=130")
+    assert np.linalg.norm(a - ref) <= 1e-4 * np.linalg.norm(ref)
+    assert np.array_equal(a, b)
+
+
 def test_gemm_dw_many_tiles():
     """dW = dY^T X with at least 512 output tiles (the head's dW) takes the
     256x128 tile; ragged N and K."""
