@@ -220,7 +220,9 @@ layup_status layup_unit_update_mix(layup_ctx* ctx, int32_t unit, const layup_hpa
  * ctx may be NULL; stream NULL = the context's update stream (or the default
  * stream without a context).  disagreement (device float, nullable, needs a
  * context) receives sum((p_updated - q)^2) summed over the tensors, taken
- * before the mix (appendix, model disagreement).  n_tensors >= 1. */
+ * before the mix (appendix, model disagreement).  n_tensors >= 1; a tensor
+ * with numel 0 is skipped and its pointers are not used (they may be NULL);
+ * with every tensor empty the disagreement is 0. */
 layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
                                     const layup_hparams* hp, float alpha, int32_t mix_mode,
                                     float* disagreement, void* stream);
@@ -354,7 +356,9 @@ layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, cons
  * a_kmajor=1, b_kmajor=1.  Contiguous dimensions and leading dimensions must
  * be multiples of 8 elements and pointers 16-byte aligned.  The float32 path
  * (layup_gemm_f32, not batched) has the same layout rules with float operands
- * and no alignment requirement; it always writes float32. */
+ * and no alignment requirement; it always writes float32.  M = 0 or N = 0 is
+ * a no-op; K = 0 writes C = bias (or 0).  Operands that are not read (A with
+ * M = 0 or K = 0, B with N = 0 or K = 0) may be NULL. */
 typedef struct {
   int32_t a_kmajor, b_kmajor;
   int64_t M, N, K;

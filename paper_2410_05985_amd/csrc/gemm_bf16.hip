@@ -798,7 +798,12 @@ std::string gemm_check(const Gemm& g, bool f32_operands) {
   if (g.M < 0 || g.N < 0 || g.K < 0) return "negative GEMM dimension";
   if (!f32_operands && !g.a_kmajor && g.b_kmajor) return "m-major A with k-major B is not supported";
   if (g.batch < 1 || g.inner < 1) return "batch and inner must be >= 1";
-  if (!g.A || !g.B || (!g.C && g.epi != EPI_UPDATE)) return "null GEMM operand";
+  // an operand is needed only when it is read (A: M, K > 0; B: N, K > 0) or
+  // written (C: M, N > 0); with K = 0 the result is the bias (or zero)
+  const bool reads = g.K > 0;
+  if ((reads && g.M > 0 && !g.A) || (reads && g.N > 0 && !g.B) ||
+      (g.M > 0 && g.N > 0 && !g.C && g.epi != EPI_UPDATE))
+    return "null GEMM operand";
   if (g.epi == EPI_UPDATE) {
     if (!g.upd.p || !g.upd.m || !g.upd.q || (g.upd.adamw && !g.upd.v)) return "update epilogue needs p, m, (v) and q";
     if (g.a_kmajor || g.b_kmajor || g.batch != 1) return "update epilogue only for dW = dY^T X";

@@ -1032,8 +1032,13 @@ layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors,
   std::vector<UMTensor> ts(n_tensors);
   for (int i = 0; i < n_tensors; ++i) {
     const layup_tensor& t = tensors[i];
-    if (!t.param || !t.grad || !t.state0 || !t.peer || t.numel < 0)
-      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": null pointer or negative size");
+    if (t.numel < 0) return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": negative size");
+    if (t.numel == 0) {  // nothing to read or write: the pointers are not used
+      ts[i] = UMTensor{};
+      continue;
+    }
+    if (!t.param || !t.grad || !t.state0 || !t.peer)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": null pointer");
     if (hp->kind == LAYUP_ADAMW && !t.state1)
       return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": AdamW needs state1");
     uintptr_t al = (uintptr_t)t.param | (uintptr_t)t.grad | (uintptr_t)t.state0 | (uintptr_t)t.peer |

@@ -239,8 +239,9 @@ hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp,
   A.trace_cap = tr.capacity;
   A.trace_step = tr.step;
   A.trace_unit = tr.unit;
-  if (chunks == 0) return hipSuccess;
-  int64_t grid = std::min<int64_t>(chunks, UM_MAX_BLOCKS);
+  // at least one block even when every tensor is empty: it still writes the
+  // disagreement partial (zero) and appends the order-trace entry
+  const int64_t grid = std::max<int64_t>(1, std::min<int64_t>(chunks, UM_MAX_BLOCKS));
   const bool dis = dis_out != nullptr;
   if (hp.kind == LAYUP_ADAMW) {
     if (dis) launch_um<1, true>(push, grid, A, chunks, stream);

@@ -100,6 +100,42 @@ def test_gemm_split_k_unaligned_columns():
     assert np.array_equal(a, b)
 
 
+@pytest.mark.parametrize("layout", ["kk", "kn", "mn"])
+def test_gemm_degenerate_sizes(layout):
+    """K = 0: C = bias (float32 and bf16 outputs, and the float32 GEMM), the
+    row sums of A are 0, and the operands, never read, may be NULL.  M = 0 or
+    N = 0: nothing is written."""
+    ak, bk = {"kk": (True, True), "kn": (True, False), "mn": (False, False)}[layout]
+    M, N = 72, 40
+    bvec = torch.from_numpy(S.normal((N,), 3)).to(DEV)
+    lda, ldb = (0 if ak else M), (0 if bk else N)
+    s = torch.cuda.current_stream()
+    for f32 in (True, False):
+        C = torch.full((M, N), float("nan"), dtype=torch.float32 if f32 else torch.bfloat16, device=DEV)
+        rs = torch.full((M,), float("nan"), dtype=torch.float32, device=DEV) if not ak else None
+        d = LU.gemm_desc(None, None, C, M, N, 0, lda, ldb, N, ak, bk, f32, bias=bvec, a_rowsum=rs)
+        LU.layup_gemm_bf16(d, s)
+        torch.cuda.synchronize()
+        want = bvec if f32 else bvec.to(torch.bfloat16)
+        assert torch.equal(C, want.expand(M, N)), f32
+        if rs is not None:
+            assert torch.equal(rs, torch.zeros_like(rs))
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device=DEV)
+    LU.layup_gemm_f32(LU.gemm_desc(None, None, C, M, N, 0, lda, ldb, N, ak, bk, True, bias=bvec), s)
+    torch.cuda.synchronize()
+    assert torch.equal(C, bvec.expand(M, N))
+    # M = 0 or N = 0: a sentinel output is left as it is
+    A = bf16_tensor((M, 64) if ak else (64, M), 5).to(DEV)
+    B = bf16_tensor((N, 64) if bk else (64, N), 6).to(DEV)
+    sentinel = torch.full((M, N), 7.0, dtype=torch.float32, device=DEV)
+    for m_, n_ in ((0, N), (M, 0)):
+        d = LU.gemm_desc(A, B, sentinel, m_, n_, 64, 64 if ak else max(m_, 8), 64 if bk else max(n_, 8),
+                         max(n_, 8), ak, bk, True)
+        LU.layup_gemm_bf16(d, s)
+    torch.cuda.synchronize()
+    assert torch.equal(sentinel, torch.full_like(sentinel, 7.0))
+
+
 def test_gemm_dw_many_tiles():
     """dW = dY^T X with at least 512 output tiles (the head's dW) takes the
     256x128 tile; ragged N and K."""

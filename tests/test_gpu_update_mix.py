@@ -113,6 +113,34 @@ def test_update_mix_multi_tensor_decay_shadow_disagreement(optim, layup_ctx):
 
 
 @pytest.mark.parametrize("optim", ["sgd", "adamw"])
+def test_update_mix_empty_tensors(optim, layup_ctx):
+    """Empty tensors are skipped, their pointers unused (NULL here): an empty
+    tensor between two others changes nothing in them, and a call whose
+    tensors are all empty still writes its disagreement (0)."""
+    e = np.zeros(0, np.float32)
+    a = S.update_mix_inputs(4099, 31, optim)
+    b = S.update_mix_inputs(517, 32, optim)
+    tensors = [(*a, 1), (e, e, e, e if optim == "adamw" else None, e, 1), (*b, 0)]
+    gpu, dis = run_gpu(tensors, optim, 0.4, step=2, dis=True, ctx=layup_ctx)
+    ref, dref = run_oracle(tensors, optim, 0.4, step=2)
+    for i in (0, 2):
+        compare(gpu[i][0], ref[i][0], 1e-5, f"p[{i}]")
+        compare(gpu[i][1], ref[i][1], 1e-5, f"m[{i}]")
+    assert gpu[1][0].size == 0
+    assert abs(dis - dref) <= 1e-5 * abs(dref), (dis, dref)
+    # every tensor empty: the disagreement output is overwritten with 0
+    out = torch.full((1,), float("nan"), dtype=torch.float32, device=DEV)
+    empty = [LU.layup_tensor(numel=0, decay=1) for _ in range(3)]
+    torch.cuda.synchronize()
+    LU.layup_layer_update_mix(layup_ctx, empty, _hp(optim), 0.5, disagreement=out,
+                              stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert out.item() == 0.0
+    with pytest.raises(RuntimeError):  # a negative size is still an error
+        LU.layup_layer_update_mix(layup_ctx, [LU.layup_tensor(numel=-1)], _hp(optim), 0.5)
+
+
+@pytest.mark.parametrize("optim", ["sgd", "adamw"])
 def test_update_mix_invariants_bit_exact(optim):
     n = 12345
     p, g, m, v, q = S.update_mix_inputs(n, 7, optim)
