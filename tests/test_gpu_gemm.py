@@ -204,10 +204,16 @@ def test_gemm_batched_attention_strides():
     (8192, 2304, 768, "kk"),    # qkv forward
     (1024, 768, 50304, "kn"),   # head dX over the vocabulary (1024 of the 8192 rows)
     (50304, 768, 1024, "mn"),   # head dW (K = 1024 of the 8192 tokens)
+    (8192, 1024, 4096, "kn"),   # GPT-2-medium fc dX
+    (4096, 1024, 8192, "mn"),   # GPT-2-medium fc dW (split K)
+    (8192, 8192, 2048, "kn"),   # 1.3B mlp-proj dX (256x256 tiles)
+    (2048, 8192, 8192, "mn"),   # 1.3B mlp-proj dW (256x256 tiles, long K)
+    (8192, 6144, 2048, "kk"),   # 1.3B qkv forward
 ])
 def test_gemm_full_size_sampled(M, N, K, layout):
-    """Full GPT-2-small backward shapes (batch 8 x 1024 tokens), checked on
-    4096 sampled outputs, each an independent float64 dot product."""
+    """Full backward shapes of the GPT-2-small, GPT-2-medium and 1.3B blocks
+    (8192 tokens), checked on 4096 sampled outputs, each an independent
+    float64 dot product."""
     ak, bk = {"kk": (True, True), "kn": (True, False), "mn": (False, False)}[layout]
     A = bf16_tensor((M, K) if ak else (K, M), 31, 0.5)
     B = bf16_tensor((N, K) if bk else (K, N), 32, 0.5)

@@ -177,3 +177,33 @@ def test_update_mix_gpt2_small_block_full_size():
         compare(pg, pr, 1e-5, "p")
         compare(mg, mr, 1e-5, "m")
         compare(vg, vr, 1e-5, "v")
+
+
+def test_update_mix_resnet50_sweep_full_size():
+    """The ResNet-50 parameter set (161 tensors, 25.6 M parameters) updated
+    and mixed unit by unit in reverse order, one launch per unit as the
+    bandwidth sweep runs it: SGD momentum 0.9, lr 0.1, weight decay 5e-5 on
+    every tensor, alpha 0.5, zero momentum; every tensor against the oracle at
+    rel 1e-5."""
+    params, grads, peer = S.resnet50_tensors()
+    units = S.resnet50_units()
+    kw = dict(lr=0.1, momentum=0.9, weight_decay=5e-5)
+    hp = _hp("sgd", 1, **kw)
+    dev = {n: dict(p=_dev(params[n].reshape(-1)), g=_dev(grads[n].reshape(-1)),
+                   m=torch.zeros(params[n].size, dtype=torch.float32, device=DEV),
+                   q=_dev(peer[n].reshape(-1))) for n in params}
+    torch.cuda.synchronize()
+    for u in reversed(units):
+        descs = [LU.layup_tensor(param=dev[n]["p"].data_ptr(), grad=dev[n]["g"].data_ptr(),
+                                 state0=dev[n]["m"].data_ptr(), peer=dev[n]["q"].data_ptr(),
+                                 numel=params[n].size, decay=1) for n in u]
+        LU.layup_layer_update_mix(None, descs, hp, 0.5, stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert sum(len(u) for u in units) == len(params) == 161 and len(units) == 54
+    for n in params:
+        p = params[n].reshape(-1)
+        ref_p, ref_m, _, _ = O.update_mix(p, grads[n].reshape(-1), np.zeros_like(p), None,
+                                          peer[n].reshape(-1), _ohp("sgd", **kw), 0.5, 1)
+        compare(dev[n]["p"].cpu().numpy(), ref_p, 1e-5, f"p {n}")
+        compare(dev[n]["m"].cpu().numpy(), ref_m, 1e-5, f"m {n}")
+
