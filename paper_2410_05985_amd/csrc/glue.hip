@@ -130,11 +130,16 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, cons
   if (row >= rows) return;
   const f32x4* xr = reinterpret_cast<const f32x4*>(x + row * d);
   const int nv = d / 4;
-  f32x4 v[NVL];
+  // the row, gain and bias are all requested before the first reduction
+  f32x4 v[NVL], gg[NVL], bb[NVL];
 #pragma unroll
   for (int j = 0; j < NVL; ++j) {
     const int i = lane + 64 * j;
-    if (i < nv) v[j] = xr[i];
+    if (i < nv) {
+      v[j] = xr[i];
+      gg[j] = reinterpret_cast<const f32x4*>(g)[i];
+      bb[j] = reinterpret_cast<const f32x4*>(b)[i];
+    }
   }
   float s = 0.f;
 #pragma unroll
@@ -157,11 +162,9 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const float* x, cons
   for (int j = 0; j < NVL; ++j) {
     const int i = lane + 64 * j;
     if (i >= nv) continue;
-    const f32x4 gg = reinterpret_cast<const f32x4*>(g)[i];
-    const f32x4 bb = reinterpret_cast<const f32x4*>(b)[i];
     u32x2 o;
-    o[0] = pack_bf2((v[j][0] - mu) * r * gg[0] + bb[0], (v[j][1] - mu) * r * gg[1] + bb[1]);
-    o[1] = pack_bf2((v[j][2] - mu) * r * gg[2] + bb[2], (v[j][3] - mu) * r * gg[3] + bb[3]);
+    o[0] = pack_bf2((v[j][0] - mu) * r * gg[j][0] + bb[j][0], (v[j][1] - mu) * r * gg[j][1] + bb[j][1]);
+    o[1] = pack_bf2((v[j][2] - mu) * r * gg[j][2] + bb[j][2], (v[j][3] - mu) * r * gg[j][3] + bb[j][3]);
     reinterpret_cast<u32x2*>(y + row * d)[i] = o;
   }
   if (lane == 0) {
