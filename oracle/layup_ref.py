@@ -39,17 +39,39 @@ Array = np.ndarray
 
 def bf16(x) -> Array:
     """Round float64 values to the nearest bfloat16 value, ties to even,
-    without going through float32 (no double rounding).  Returns float64."""
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)                      # x = m * 2**e, 0.5 <= |m| < 1
-    r = np.ldexp(np.rint(np.ldexp(m, 8)), e - 8)   # 8 significant bits
-    tiny = np.abs(x) < 2.0 ** -126          # bfloat16 subnormals: spacing 2**-133
-    if np.any(tiny):
-        r = np.where(tiny, np.ldexp(np.rint(np.ldexp(x, 133)), -133), r)
-    big = np.abs(r) >= 2.0 ** 128           # beyond the largest finite bfloat16
-    if np.any(big):
-        r = np.where(big, np.copysign(np.inf, x), r)
-    return r
+    without going through float32 (no double rounding).  Returns float64.
+
+    A bfloat16 keeps 8 significant bits.  For a float64 in the normal range
+    of bfloat16 that means dropping the low 45 of its 52 stored mantissa bits
+    with round-to-nearest-even, done on the integer bit pattern: add half an
+    ulp minus one, plus the lowest kept bit (the tie goes to the even
+    neighbour), then clear the dropped bits; a carry out of the mantissa
+    moves the exponent up, which is the correct rounding across a binade.
+    Below 2**-126 bfloat16 is subnormal with spacing 2**-133."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    xf, of = x.reshape(-1), out.reshape(-1)
+    step = 1 << 17                                        # slices small enough to stay in cache
+    for s in range(0, xf.size, step):
+        xs = xf[s: s + step]
+        bits = xs.view(np.uint64)
+        r = (bits >> np.uint64(45)) & np.uint64(1)        # lowest kept bit
+        r += bits
+        r += np.uint64((1 << 44) - 1)
+        r &= ~np.uint64((1 << 45) - 1)
+        of[s: s + step] = r.view(np.float64)
+        ax = np.abs(xs)
+        odd = ~(ax >= 2.0 ** -126) | (ax >= 2.0 ** 127)  # subnormal, zero, NaN, near or past overflow
+        if np.any(odd):
+            i = np.nonzero(odd)[0]
+            xo = xs[i]
+            ro = of[s + i]
+            tiny = np.abs(xo) < 2.0 ** -126               # bfloat16 subnormals: spacing 2**-133
+            ro = np.where(tiny, np.rint(np.where(tiny, xo, 0.0) * 2.0 ** 133) * 2.0 ** -133, ro)
+            ro = np.where(np.abs(ro) >= 2.0 ** 128, np.copysign(np.inf, xo), ro)  # past the largest bfloat16
+            ro = np.where(np.isnan(xo), xo, ro)
+            of[s + i] = ro
+    return out
 
 
 def f32(x) -> Array:
@@ -442,6 +464,29 @@ def gpt_block_bwd(params, c, dx, l, bsz, t, n_head, rnd: Callable = bf16):
     return g, dh_res + dln1
 
 
+def gpt_head_bwd(params, dlog, xf, xL, rnd: Callable = bf16):
+    """Backward of the top unit: the tied output head (logits = xf wte^T)
+    and the final LayerNorm, given the logit gradient.  Returns (grads of
+    lnf.g and lnf.b, dx at the last block's output, the head's contribution
+    to the wte gradient)."""
+    dlog = np.asarray(dlog, np.float64)
+    xf = np.asarray(xf, np.float64)
+    dxf = dlog @ rnd(np.asarray(params["wte"], np.float64))
+    wte_head = dlog.T @ xf
+    dx, dg, db = layernorm_bwd(dxf, np.asarray(xL, np.float64), params["lnf.g"])
+    return {"lnf.g": dg, "lnf.b": db}, dx, wte_head
+
+
+def gpt_embed_bwd(dx, idx, wte_head, bsz, t):
+    """Backward of the input embeddings x0 = wte[tok] + wpe[pos]: wte
+    collects the head's gradient plus dx scattered over the input tokens;
+    wpe sums dx over the batch per position."""
+    dx = np.asarray(dx, np.float64)
+    dwte = np.asarray(wte_head, np.float64).copy()
+    np.add.at(dwte, np.asarray(idx), dx)
+    return {"wte": dwte, "wpe": dx.reshape(bsz, t, -1).sum(axis=0)}
+
+
 def gpt_step(params, m, v, peer, tokens, n_head, hp, alpha, t=1, rnd: Callable = bf16,
              update: bool = True, store: Callable = f32, push: bool = False):
     """One layer-wise LayUp step of a GPT stack.  ``params``, ``m``, ``v`` are
@@ -465,23 +510,19 @@ def gpt_step(params, m, v, peer, tokens, n_head, hp, alpha, t=1, rnd: Callable =
                                  lambda n: n in decay, store, push)
 
     # unit L+1: output head (tied wte) and final LayerNorm
-    wte16 = rnd(params_f["wte"])
-    dxf = dlog @ wte16
-    wte_head = dlog.T @ cache["xf"]
-    dx, grads["lnf.g"], grads["lnf.b"] = layernorm_bwd(dxf, cache["xL"], params_f["lnf.g"])
-    grads["lnf.g"], grads["lnf.b"] = store(grads["lnf.g"]), store(grads["lnf.b"])
+    g, dx, wte_head = gpt_head_bwd(params_f, dlog, cache["xf"], cache["xL"], rnd)
+    for k_, a_ in g.items():
+        grads[k_] = store(a_)
     apply(n_layer + 1)
     for l in range(n_layer - 1, -1, -1):
         g, dx = gpt_block_bwd(params_f, cache[l], dx, l, bsz, t_len, n_head, rnd)
         for k_, a_ in g.items():
             grads[k_] = store(a_)
         apply(l + 1)
-    # unit 0: embeddings.  wte collects the head gradient and the scatter of
-    # dx over the input tokens; wpe sums dx over the batch per position.
-    dwte = wte_head.copy()
-    np.add.at(dwte, cache["idx"], dx)
-    grads["wte"] = store(dwte)
-    grads["wpe"] = store(dx.reshape(bsz, t_len, -1).sum(axis=0))
+    # unit 0: embeddings
+    g = gpt_embed_bwd(dx, cache["idx"], wte_head, bsz, t_len)
+    for k_, a_ in g.items():
+        grads[k_] = store(a_)
     apply(0)
     return loss, grads, trace, dis
 

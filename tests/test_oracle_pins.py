@@ -171,6 +171,46 @@ def test_bf16_special_values():
     assert O.bf16(A([x]))[0] == 1 + 2 ** -7
 
 
+def _bf16_nearest_exact(x: float) -> float:
+    """Plain definition on one value: enumerate the bfloat16 grid around x
+    (8 significant bits; spacing 2**-133 below 2**-126) and take the
+    nearest value in exact rational arithmetic, ties to the even
+    significand; past the largest finite value the result is infinite."""
+    from fractions import Fraction
+    if x == 0:
+        return x
+    ax = Fraction(abs(x))
+    e = max(math.frexp(abs(x))[1] - 8, -133)          # grid spacing 2**e
+    lo = (ax / Fraction(2) ** e).__floor__()
+    cands = [lo, lo + 1]
+    best = min(cands, key=lambda k: (abs(Fraction(k) * Fraction(2) ** e - ax), k % 2))
+    val = float(Fraction(best) * Fraction(2) ** e)
+    if val >= 2.0 ** 128:
+        val = math.inf
+    return math.copysign(val, x)
+
+
+def test_bf16_float64_brute_force():
+    """float64 inputs with bits far below the bfloat16 grid (no double
+    rounding), near ties, across the subnormal and overflow boundaries, in
+    a 2-D array (shape kept), against the exact nearest-even definition."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(3000) * 10.0 ** rng.integers(-42, 39, 3000)
+    k = rng.integers(0, 256, 600).astype(np.float64) + 0.5
+    e = rng.integers(-141, 121, 600).astype(np.float64)
+    ties = k * 2.0 ** e
+    x = np.concatenate([x, ties, np.nextafter(ties, 0), np.nextafter(ties, np.inf), -ties,
+                        [(2 - 2 ** -8) * 2.0 ** 127, (2 - 2 ** -9) * 2.0 ** 127,
+                         np.nextafter((2 - 2 ** -9) * 2.0 ** 127, 0), 2.0 ** -126, 2.0 ** -127,
+                         np.nextafter(2.0 ** -126, 0), 2.0 ** -134, np.nextafter(2.0 ** -134, 1), 5e-324,
+                         0.0, -0.0, 1.0]])
+    x = x.reshape(-1, 2)
+    got = O.bf16(x)
+    assert got.shape == x.shape
+    want = np.array([_bf16_nearest_exact(float(v)) for v in x.reshape(-1)]).reshape(x.shape)
+    assert np.array_equal(got, want)
+
+
 def test_causal_logsumexp_brute_force_and_softmax():
     """The causal log-sum-exp (the softmax normaliser the fused attention
     stores) against a plain loop with math.fsum, and exp(s - lse) against the
