@@ -335,8 +335,13 @@ layup_status layup_push_sum_receive(double* w, int32_t n_workers, int32_t sender
  * pre-activation (bf16), 8 = GELU out (bf16), 9 = final LN out (bf16),
  * 10 = logit gradient (bf16), 11 = final residual (f32), 12 = base-2
  * log-sum-exp of each query's scaled causal scores (f32, [B][H][T]; fused
- * attention, head width 32, 64 or 128, only).  layer is the block index for
- * 0..8 and 12.  dtype_out: 0 = f32, 1 = bf16.  Asking for an activation the
+ * attention, head width 32, 64 or 128, only), 13 = float32 gradient of the
+ * loss with respect to the input of the unit whose backward ran last, i.e.
+ * the output gradient the next unit's backward consumes ([batch*seq,
+ * d_model]; Algorithm 1 "Backward pass at layer l" hands it down; valid
+ * after layup_layer_backward of a unit >= 1 and until the next backward or
+ * forward, LAYUP_ERR_STATE otherwise).  layer is the block index for 0..8
+ * and 12.  dtype_out: 0 = f32, 1 = bf16.  Asking for an activation the
  * configuration does not store is LAYUP_ERR_INVALID_ARG. */
 layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, const void** ptr,
                               int64_t* numel, int32_t* dtype_out);

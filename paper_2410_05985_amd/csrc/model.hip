@@ -172,6 +172,7 @@ struct layup_ctx {
   int next_backward = -1;
   std::vector<char> backward_done;
   int32_t step_index = 0;  // value written to the trace
+  bool dx_valid = false;   // dx[cur_dx] holds the input gradient of the last backwarded unit
   // workspace
   size_t ws_bytes = 0;
   std::vector<BlockActs> acts;
@@ -970,6 +971,7 @@ layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x
   if (ctx->have_join) HIPCHK(ctx, hipStreamWaitEvent(ctx->sc, ctx->ev_join, 0), "wait join");
   HIPCHK(ctx, hipEventRecord(ctx->ev_start, ctx->sc), "record step start");
   ctx->timeline_valid = false;
+  ctx->dx_valid = false;
   ctx->tokens = tokens;
   layup_status st = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 ? gpt_forward(ctx, tokens, loss_out)
                                                             : mlp_forward(ctx, tokens, x, loss_out);
@@ -997,6 +999,7 @@ layup_status layup_layer_backward(layup_ctx* ctx, int32_t unit) {
     HIPCHK(ctx, hipEventRecord(ctx->ev_unit[unit], ctx->su), "record unit event");
   }
   ctx->backward_done[unit] = 1;
+  ctx->dx_valid = ctx->cfg.model == LAYUP_MODEL_GPT_BF16 && unit >= 1;
   ctx->next_backward--;
   if (ctx->next_backward < 0) ctx->forward_done = false;
   return LAYUP_OK;
@@ -1236,6 +1239,10 @@ layup_status layup_activation(layup_ctx* ctx, int32_t which, int32_t layer, cons
     case 12:
       if (!A->lse) return fail(ctx, LAYUP_ERR_INVALID_ARG, "the log-sum-exp is stored by the fused attention only (head width 32, 64 or 128)");
       p = A->lse; n = (int64_t)g.batch * g.n_head * g.seq; dt = 0; break;
+    case 13:
+      if (!ctx->dx_valid)
+        return fail(ctx, LAYUP_ERR_STATE, "no unit above the embeddings has been backpropagated since the forward");
+      p = ctx->dx[ctx->cur_dx]; n = N * d; dt = 0; break;
     default: return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown activation");
   }
   *ptr = p;

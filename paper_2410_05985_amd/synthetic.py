@@ -112,6 +112,20 @@ GPT_TEST_W832 = GPTConfig(n_layer=1, d_model=832, n_head=13, d_ff=256, seq=64, b
 GPT_TEST_W1088 = GPTConfig(n_layer=1, d_model=1088, n_head=17, d_ff=256, seq=64, batch=2,
                            vocab=250, name="gpt-test-w1088")
 
+# Four blocks: the backward's dY operands (double-buffered by block parity)
+# are reused from the third block down, under both streams.
+GPT_TEST4 = GPTConfig(n_layer=4, d_model=128, n_head=2, d_ff=512, seq=128, batch=2, vocab=1000,
+                      name="gpt-test-4blocks")
+# GPT-2-small's own widths (768 features, 12 heads of 64, MLP 3072, 1024
+# tokens per sequence, the 50257-token vocabulary) with two blocks and two
+# sequences: the LayerNorm, cross-entropy and attention kernels the full
+# stack runs, at a size the oracle finishes in seconds.
+GPT2_SMALL_2L = GPTConfig(n_layer=2, d_model=768, n_head=12, d_ff=3072, seq=1024, batch=2,
+                          name="gpt2-small-width-2blocks")
+# Head width 128 over 2048 tokens: the attention path of the 1.3B stack.
+GPT_TEST_T2048 = GPTConfig(n_layer=1, d_model=256, n_head=2, d_ff=512, seq=2048, batch=1, vocab=300,
+                           name="gpt-test-t2048-dh128")
+
 RESNET50_UPDATE = dict(lr=0.1, momentum=0.9, weight_decay=5e-5, alpha=0.5)
 
 # ------------------------------------------------------------ param specs

@@ -1,0 +1,53 @@
+"""Shared set-up of the GPU tests of the GPT stacks: a model loaded with the
+seeded parameters, tokens and peer replicas, and the hyperparameters in the
+library's and the oracle's form.  Also the oracle's per-block cache built from
+the activations the GPU saved, for teacher-forced checks (both sides start a
+unit's backward from the same stored values)."""
+import math
+
+import numpy as np
+
+import oracle as O
+from paper_2410_05985_amd import synthetic as S
+
+
+def gpt_setup(cfg, two_streams=True, n_peers=1):
+    from paper_2410_05985_amd import layup as LU
+    params = S.gpt_params(cfg)
+    tokens = S.gpt_tokens(cfg)
+    peers = [S.gpt_peer(cfg, params, slot=i) for i in range(n_peers)]
+    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch,
+                       cfg.vocab, n_peers)
+    m = LU.Model(lc, "adamw", two_streams=two_streams)
+    m.load("params", params)
+    for i, p in enumerate(peers):
+        m.load("peers", p, slot=i)
+    return params, tokens, peers, m
+
+
+def gpt_hp(cfg, step=1):
+    from paper_2410_05985_amd import layup as LU
+    return (LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, step),
+            dict(optim="adamw", lr=cfg.lr, weight_decay=cfg.weight_decay, beta1=cfg.beta1,
+                 beta2=cfg.beta2, eps=cfg.eps))
+
+
+def block_cache_from_gpu(m, cfg, l):
+    """The oracle's cache of block l (gpt_forward's keys) filled with the
+    activations the GPU stored.  The fused attention keeps no probabilities:
+    they are taken from the GPU's stored q and k by the oracle's causal
+    softmax, rounded to bfloat16 at the same storage point as in the oracle's
+    forward; the unfused path's stored probabilities are used as they are."""
+    N, d, F = cfg.batch * cfg.seq, cfg.d_model, cfg.d_ff
+    H, T, B = cfg.n_head, cfg.seq, cfg.batch
+    dh = d // H
+    act = lambda w, shape: m.activation(w, l).astype(np.float64).reshape(shape)
+    c = {"x": act(0, (N, d)), "a": act(1, (N, d)), "qkv": act(2, (N, 3 * d)), "o": act(4, (N, d)),
+         "h": act(5, (N, d)), "a2": act(6, (N, d)), "f": act(7, (N, F)), "gl": act(8, (N, F))}
+    if dh in (32, 64, 128):
+        q = O._heads(c["qkv"][:, :d], B, T, H, dh)
+        k = O._heads(c["qkv"][:, d:2 * d], B, T, H, dh)
+        c["P"] = O.bf16(O.causal_softmax((q @ k.swapaxes(-1, -2)) * (1.0 / math.sqrt(dh))))
+    else:
+        c["P"] = act(3, (B, H, T, T))
+    return c

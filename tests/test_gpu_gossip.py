@@ -269,6 +269,51 @@ def test_after_backward_schedule_equals_layerwise_and_lands_later():
     assert max(a["ready"]) == a["ready"][0] and max(b["ready"]) == b["ready"][0]
 
 
+def test_drift_of_the_two_schedules_gpt2_small():
+    """Section 3.2's drift at GPT-2-small's full size, from the HIP-event
+    timeline of the third step of each schedule.  The drift of a unit is the
+    delay from its gradient being ready to its update being applied.
+
+    * After the whole backward pass, every update lands after the last
+      gradient, and the delay grows with the unit's distance from the input
+      over the blocks and the top unit (a unit's gradient is ready one
+      unit-backward earlier than the one below it, and updates take a small
+      fraction of a unit-backward).  The embeddings' unit is left out: its
+      gradient comes last and its update is the largest.
+    * The summed delay D lies within [0.5, 1.25] of the paper's model
+      beta T (L + 1) / 2, with beta T the measured backward time and L the
+      number of units: the model takes every unit's backward to last
+      beta T / L, while here the top unit (the tied head) takes longer and the
+      embeddings' unit much less.
+    * The layer-wise schedule's summed delay is a small fraction of it."""
+    cfg = S.GPT2_SMALL
+    params = S.gpt_params(cfg)
+    peer = S.gpt_peer(cfg, params)
+    tokens = _dev(S.gpt_tokens(cfg))
+    res = {}
+    for sched in (LU.LAYUP_SCHEDULE_LAYERWISE, LU.LAYUP_SCHEDULE_AFTER_BACKWARD):
+        m = _gpt_model(cfg, params, peer)
+        for step in (1, 2, 3):
+            hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, step)
+            LU.layup_step_ex(m.ctx, tokens, None, hp, cfg.alpha, schedule=sched)
+        res[sched] = LU.layup_unit_timeline(m.ctx, m.n_units)
+        U = m.n_units
+        m.close()
+        del m
+    fwd, ready, applied = res[LU.LAYUP_SCHEDULE_AFTER_BACKWARD]
+    delay = [applied[u] - ready[u] for u in range(U)]
+    assert min(applied) >= max(ready) == ready[0]
+    for u in range(1, U - 1):
+        assert delay[u + 1] > delay[u], (u, delay)
+    d_after = sum(delay)
+    beta_t = ready[0] - fwd
+    model = beta_t * (U + 1) / 2
+    assert 0.5 * model <= d_after <= 1.25 * model, (d_after, model)
+    fwd_l, ready_l, applied_l = res[LU.LAYUP_SCHEDULE_LAYERWISE]
+    d_layer = sum(applied_l[u] - ready_l[u] for u in range(U))
+    assert 0 < d_layer < 0.2 * d_after, (d_layer, d_after)
+
+
 def test_step_ex_argument_checks():
     cfg = S.GPT_TEST
     params = S.gpt_params(cfg)

@@ -10,6 +10,7 @@ import pytest
 
 import oracle as O
 from paper_2410_05985_amd import synthetic as S
+from tests.gpt_cases import gpt_hp, gpt_setup
 from tests.parity import compare, compare_chained
 
 pytestmark = pytest.mark.gpu
@@ -84,25 +85,6 @@ def test_mlp_two_streams_equal_one_stream():
 
 # ------------------------------------------------------------------ GPT
 
-def gpt_setup(cfg, two_streams=True, n_peers=1):
-    params = S.gpt_params(cfg)
-    tokens = S.gpt_tokens(cfg)
-    peers = [S.gpt_peer(cfg, params, slot=i) for i in range(n_peers)]
-    lc = LU.gpt_config(cfg.n_layer, cfg.d_model, cfg.n_head, cfg.d_ff, cfg.seq, cfg.batch,
-                       cfg.vocab, n_peers)
-    m = LU.Model(lc, "adamw", two_streams=two_streams)
-    m.load("params", params)
-    for i, p in enumerate(peers):
-        m.load("peers", p, slot=i)
-    return params, tokens, peers, m
-
-
-def gpt_hp(cfg, step=1):
-    return (LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, step),
-            dict(optim="adamw", lr=cfg.lr, weight_decay=cfg.weight_decay, beta1=cfg.beta1,
-                 beta2=cfg.beta2, eps=cfg.eps))
-
-
 def check_adamw_params(got, ref, g_ref, lr, alpha, name):
     """After an AdamW step from zero moments the local update is
     -lr * g/(|g| + eps): where the two sides' gradients agree in sign the
@@ -120,7 +102,8 @@ def check_adamw_params(got, ref, g_ref, lr, alpha, name):
                       + 1e-5 * (np.abs(ref[loose]) + 1e-3)), name
 
 
-@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48],
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48,
+                                 S.GPT2_SMALL_2L, S.GPT_TEST_T2048],
                          ids=lambda c: c.name)
 def test_gpt_forward_activations(cfg):
     """Saved forward activations against the oracle's forward (bf16 storage
@@ -160,19 +143,34 @@ def test_gpt_forward_activations(cfg):
 
 
 @pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48,
-                                 S.GPT_TEST_W832, S.GPT_TEST_W1088],
+                                 S.GPT_TEST_W832, S.GPT_TEST_W1088, S.GPT_TEST4, S.GPT2_SMALL_2L,
+                                 S.GPT_TEST_T2048],
                          ids=lambda c: c.name)
 def test_gpt_step_parity(cfg):
     """One layer-wise step, chained: every gradient at rel 2e-2 (bf16 GEMM
     operands, float32 accumulation), AdamW moments and the mixed parameters as
-    described in check_adamw_params, order trace exact."""
+    described in check_adamw_params, order trace exact; then the update
+    teacher-forced (the oracle's update of the GPU's gradients) at 1e-5."""
+    _step_parity(cfg, LU.LAYUP_SCHEDULE_LAYERWISE)
+
+
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST4], ids=lambda c: c.name)
+def test_after_backward_schedule_matches_oracle(cfg):
+    """The comparison schedule of section 3.2 (every update after the whole
+    backward pass) against the oracle's step directly, with the same bars
+    as the layer-wise step: on one worker the two schedules compute the same
+    step, so the oracle's layer-wise step is the reference for both."""
+    _step_parity(cfg, LU.LAYUP_SCHEDULE_AFTER_BACKWARD)
+
+
+def _step_parity(cfg, schedule):
     params, tokens, peers, m = gpt_setup(cfg)
     hp, ohp = gpt_hp(cfg)
     td = torch.from_numpy(tokens).to(DEV)
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     dis = torch.zeros(m.n_units, dtype=torch.float32, device=DEV)
     torch.cuda.synchronize()
-    LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0, loss, dis)
+    LU.layup_step_ex(m.ctx, td, None, hp, cfg.alpha, schedule=schedule, loss_out=loss, disagreement=dis)
     op = {k: v.astype(np.float64) for k, v in params.items()}
     om = {k: np.zeros_like(v) for k, v in op.items()}
     ov = {k: np.zeros_like(v) for k, v in op.items()}
@@ -201,14 +199,31 @@ def test_gpt_step_parity(cfg):
     dgpu = dis.cpu().numpy()
     for u in range(n_units):
         assert abs(dgpu[u] - odis[u]) <= 5e-2 * odis[u] + 1e-12, (u, dgpu[u], odis[u])
+    # teacher-forced update: the oracle's update+mix of the GPU's own
+    # gradients from the step's starting state gives the GPU's parameters
+    # and moments to rel 1e-5, element by element
+    tp = {k: v.astype(np.float64) for k, v in params.items()}
+    tm = {k: np.zeros_like(v) for k, v in tp.items()}
+    tv = {k: np.zeros_like(v) for k, v in tp.items()}
+    gg = {k: a.astype(np.float64) for k, a in g.items()}
+    O.gpt_update_units(tp, gg, tm, tv, opeer, cfg.n_layer, ohp, cfg.alpha, t=1)
+    for k in tp:
+        shp = got_p[k].shape
+        compare(got_p[k], tp[k].reshape(shp), 1e-5, f"teacher-forced param {k}")
+        compare(got_m[k], tm[k].reshape(shp), 1e-5, f"teacher-forced m {k}")
+        compare(got_v[k], tv[k].reshape(shp), 1e-5, f"teacher-forced v {k}")
     m.close()
 
 
-def test_gpt_two_streams_equal_one_stream_and_repeatable():
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST4, S.GPT2_SMALL], ids=lambda c: c.name)
+def test_gpt_two_streams_equal_one_stream_and_repeatable(cfg):
     """Two-stream overlap vs serialized schedule and two identical runs:
-    bitwise identical parameters, moments and gradients (race detector; no
-    float atomics anywhere on the path)."""
-    cfg = S.GPT_TEST
+    bitwise identical parameters, moments, gradients and bf16 weight copies
+    after two steps (race detector; no float atomics anywhere on the path).
+    With four or more blocks the dY operands of the dW GEMMs, double-buffered
+    by block parity, are overwritten two blocks later while the update
+    stream may still read them: a missing or misplaced wait changes bits.
+    GPT-2-small runs all twelve blocks at full size."""
     outs = []
     for two in (True, False, True):
         params, tokens, peers, m = gpt_setup(cfg, two)
@@ -219,12 +234,12 @@ def test_gpt_two_streams_equal_one_stream_and_repeatable():
             hp.step = s + 1
             LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0)
         m.synchronize()
-        outs.append([t.cpu().numpy().copy() for t in (m.params, m.m, m.v, m.grads)])
+        outs.append([t.clone() for t in (m.params, m.m, m.v, m.grads, m.params_bf16)])
         m.close()
-    for a, b in zip(outs[0], outs[1]):
-        assert np.array_equal(a, b)
-    for a, b in zip(outs[0], outs[2]):
-        assert np.array_equal(a, b)
+        del m
+    for run in (1, 2):
+        for name, a, b in zip(("params", "m", "v", "grads", "bf16 copy"), outs[0], outs[run]):
+            assert torch.equal(a, b), (run, name)
 
 
 def test_gpt_manual_unit_calls_match_step():

@@ -1,0 +1,130 @@
+"""Teacher-forced parity, unit by unit (Algorithm 1, "Backward pass at layer
+l", "Local Update" and "Peer Update"): each unit's backward is checked on its
+own, from the very values the GPU handed it -- the gradient with respect to
+the unit's output and the activations the forward stored -- so that no
+difference from an earlier unit can hide or excuse one in this unit.  Every
+gradient and the unit's input gradient must match the oracle element by
+element at rel 2e-2 (bf16 GEMM operands, float32 accumulation).  The
+update+mix is checked the same way: the oracle's update applied to the GPU's
+own gradients must give the GPU's parameters, moments and disagreement to
+rel 1e-5, over two steps.
+
+The chained comparisons (oracle and GPU each running the whole step from
+the same inputs) are in test_gpu_step.py."""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2410_05985_amd import synthetic as S
+from tests.gpt_cases import block_cache_from_gpu, gpt_hp, gpt_setup
+from tests.parity import compare
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+from paper_2410_05985_amd import layup as LU  # noqa: E402
+
+DEV = "cuda"
+GRAD_RTOL = 2e-2
+UPDATE_RTOL = 1e-5
+
+TEACHER_CASES = [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48, S.GPT_TEST_W832,
+                 S.GPT_TEST_LONG, S.GPT_TEST4, S.GPT2_SMALL_2L, S.GPT_TEST_T2048]
+
+
+@pytest.mark.parametrize("cfg", TEACHER_CASES, ids=lambda c: c.name)
+def test_unit_backward_teacher_forced(cfg):
+    """Forward once; then for every unit from the top down: run its backward
+    on the GPU, give the oracle the same output gradient and stored
+    activations, and compare the unit's parameter gradients and its input
+    gradient per element."""
+    params, tokens, peers, m = gpt_setup(cfg)
+    hp, _ = gpt_hp(cfg)
+    pf = {k: v.astype(np.float64) for k, v in params.items()}
+    N, d, V = cfg.batch * cfg.seq, cfg.d_model, cfg.vocab
+    td = torch.from_numpy(tokens).to(DEV)
+    torch.cuda.synchronize()
+    LU.layup_forward(m.ctx, td, None, None)
+    m.synchronize()
+    Vp = (V + 63) // 64 * 64
+    dlog = m.activation(10).astype(np.float64).reshape(N, Vp)
+    # padding columns of the logit gradient are zero (masked logits)
+    assert not np.any(dlog[:, V:]), "non-zero gradient in padding columns"
+    dlog = dlog[:, :V]
+    xf = m.activation(9).astype(np.float64).reshape(N, d)
+    xL = m.activation(11).astype(np.float64).reshape(N, d)
+    with pytest.raises(LU.LayupError):
+        m.activation(13)                       # no unit backpropagated yet
+    # top unit: tied head and final LayerNorm
+    U = cfg.n_layer + 2
+    LU.layup_layer_backward(m.ctx, U - 1)
+    LU.layup_unit_update_mix(m.ctx, U - 1, hp, cfg.alpha, 0)
+    g_ref, dx_ref, wte_head = O.gpt_head_bwd(pf, dlog, xf, xL)
+    g = m.read("grads")
+    for k, ref in g_ref.items():
+        compare(g[k], ref, GRAD_RTOL, f"unit {U - 1} grad {k}")
+    dx = m.activation(13).astype(np.float64).reshape(N, d)
+    compare(dx, dx_ref, GRAD_RTOL, f"unit {U - 1} input gradient")
+    # the blocks, each from the GPU's own output gradient
+    for l in range(cfg.n_layer - 1, -1, -1):
+        u = l + 1
+        c = block_cache_from_gpu(m, cfg, l)
+        LU.layup_layer_backward(m.ctx, u)
+        LU.layup_unit_update_mix(m.ctx, u, hp, cfg.alpha, 0)
+        g_ref, dx_ref = O.gpt_block_bwd(pf, c, dx, l, cfg.batch, cfg.seq, cfg.n_head)
+        g = m.read("grads")
+        for k, ref in g_ref.items():
+            compare(g[k], ref.reshape(g[k].shape), GRAD_RTOL, f"unit {u} grad {k}")
+        dx = m.activation(13).astype(np.float64).reshape(N, d)
+        compare(dx, dx_ref, GRAD_RTOL, f"unit {u} input gradient")
+    # embeddings: the head's part of the tied wte gradient plus the scatter
+    # of the bottom block's input gradient
+    LU.layup_layer_backward(m.ctx, 0)
+    LU.layup_unit_update_mix(m.ctx, 0, hp, cfg.alpha, 0)
+    g_ref = O.gpt_embed_bwd(dx, tokens[:, :cfg.seq].reshape(-1), wte_head, cfg.batch, cfg.seq)
+    g = m.read("grads")
+    for k, ref in g_ref.items():
+        compare(g[k], ref, GRAD_RTOL, f"unit 0 grad {k}")
+    assert m.read_trace() == [(0, u) for u in range(U - 1, -1, -1)]
+    m.close()
+
+
+@pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST4, S.GPT2_SMALL_2L],
+                         ids=lambda c: c.name)
+def test_update_mix_teacher_forced_two_steps(cfg):
+    """Two layer-wise steps.  After each, the oracle applies its update+mix
+    (AdamW, then the average with the peer slot) unit by unit in reverse
+    order to the GPU's own gradients and the state the GPU started the step
+    from; parameters, both moments and the per-unit disagreement must match
+    per element at rel 1e-5, and the bf16 weight copy must be the
+    nearest-even bf16 of the new float32 weights."""
+    params, tokens, peers, m = gpt_setup(cfg)
+    _, ohp = gpt_hp(cfg)
+    td = torch.from_numpy(tokens).to(DEV)
+    dis = torch.zeros(m.n_units, dtype=torch.float32, device=DEV)
+    peer = {k: v.astype(np.float64) for k, v in peers[0].items()}
+    p0 = {k: v.astype(np.float64) for k, v in params.items()}
+    m0 = {k: np.zeros_like(v) for k, v in p0.items()}
+    v0 = {k: np.zeros_like(v) for k, v in p0.items()}
+    for step in (1, 2):
+        hp, _ = gpt_hp(cfg, step)
+        torch.cuda.synchronize()
+        LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0, None, dis)
+        g = {k: a.astype(np.float64) for k, a in m.read("grads").items()}
+        trace, odis = O.gpt_update_units(p0, g, m0, v0, peer, cfg.n_layer, ohp, cfg.alpha, t=step)
+        got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
+        for k in p0:
+            shp = got_p[k].shape
+            compare(got_p[k], p0[k].reshape(shp), UPDATE_RTOL, f"step {step} param {k}")
+            compare(got_m[k], m0[k].reshape(shp), UPDATE_RTOL, f"step {step} m {k}")
+            compare(got_v[k], v0[k].reshape(shp), UPDATE_RTOL, f"step {step} v {k}")
+        dgpu = dis.cpu().numpy().astype(np.float64)
+        compare(dgpu, np.array([odis[u] for u in range(m.n_units)]), UPDATE_RTOL, f"step {step} disagreement")
+        assert m.read_trace()[-m.n_units:] == [(step - 1, u) for u in trace]
+        p16 = (m.params_bf16.to(torch.int32) << 16).view(torch.float32).cpu().numpy()
+        assert np.array_equal(p16, O.bf16(m.params.cpu().numpy().astype(np.float64)))
+        # the next step starts from the GPU's state (identical to p0/m0/v0 up
+        # to the float32 rounding checked above)
+        p0 = {k: a.astype(np.float64) for k, a in got_p.items()}
+        m0 = {k: a.astype(np.float64) for k, a in got_m.items()}
+        v0 = {k: a.astype(np.float64) for k, a in got_v.items()}
+    m.close()
