@@ -8,6 +8,7 @@ import math
 import numpy as np
 
 import oracle as O
+from oracle import layup_ref as OR
 from paper_2410_05985_amd import synthetic as S
 
 
@@ -45,8 +46,8 @@ def block_cache_from_gpu(m, cfg, l):
     c = {"x": act(0, (N, d)), "a": act(1, (N, d)), "qkv": act(2, (N, 3 * d)), "o": act(4, (N, d)),
          "h": act(5, (N, d)), "a2": act(6, (N, d)), "f": act(7, (N, F)), "gl": act(8, (N, F))}
     if dh in (32, 64, 128):
-        q = O._heads(c["qkv"][:, :d], B, T, H, dh)
-        k = O._heads(c["qkv"][:, d:2 * d], B, T, H, dh)
+        q = OR._heads(c["qkv"][:, :d], B, T, H, dh)
+        k = OR._heads(c["qkv"][:, d:2 * d], B, T, H, dh)
         c["P"] = O.bf16(O.causal_softmax((q @ k.swapaxes(-1, -2)) * (1.0 / math.sqrt(dh))))
     else:
         c["P"] = act(3, (B, H, T, T))

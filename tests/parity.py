@@ -36,10 +36,16 @@ def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0, exact=None):
     outside cap * rtol * (|ref| + rms).
 
     ``exact``, when given, is the oracle's result with no storage rounding
-    (exact arithmetic).  How often the bf16-storage oracle itself lands
-    beyond rtol from it measures the spread that bf16 storage alone causes;
-    the GPU, a second bf16-storage pipeline, may have as many elements
-    beyond rtol from the oracle as the oracle has from exact arithmetic."""
+    (exact arithmetic); it measures the spread that bf16 storage alone
+    causes.  The GPU is a second bf16-storage pipeline whose rounding errors
+    are independent of the oracle's and alike in size: with E exact, R the
+    oracle and G the GPU, |G - R| <= |G - E| + |R - E|, so G is more than
+    rtol from R only where one of the two is more than rtol/2 from E.  The
+    GPU may therefore have up to twice as many elements beyond rtol as the
+    oracle has beyond rtol/2 from exact arithmetic, and its worst element
+    may be up to twice the oracle's worst distance from exact arithmetic.
+    (The strict, per-element check is the teacher-forced one, where both
+    sides start every unit from the same stored values.)"""
     gpu = np.asarray(gpu, np.float64)
     ref = np.asarray(ref, np.float64)
     assert gpu.shape == ref.shape, (name, gpu.shape, ref.shape)
@@ -54,10 +60,15 @@ def compare_chained(gpu, ref, rtol, name="", frac=1e-3, cap=5.0, exact=None):
     worst = float(ratio.max())
     assert normwise <= rtol, f"{name}: normwise {normwise:.3e} > {rtol}"
     allowed = frac * ratio.size
+    worst_allowed = cap * rtol
     if exact is not None:
         exact = np.asarray(exact, np.float64)
         assert exact.shape == ref.shape, (name, exact.shape, ref.shape)
-        allowed = max(allowed, int(np.sum(np.abs(exact - ref) / np.maximum(scale, 1e-300) > rtol)))
-    assert n_out <= allowed, f"{name}: {n_out}/{ratio.size} elements beyond {rtol} (allowed {allowed:.0f})"
-    assert worst <= cap * rtol, f"{name}: worst element {worst:.3e} > {cap * rtol}"
+        spread = np.abs(exact - ref) / np.maximum(scale, 1e-300)
+        allowed = max(allowed, 2 * int(np.sum(spread > rtol / 2)))
+        worst_allowed = max(worst_allowed, 2 * float(spread.max()))
+    i = int(np.argmax(ratio))
+    where = f"worst at flat index {i}: gpu={gpu.flat[i]!r} ref={ref.flat[i]!r} scale={scale.flat[i]:.3e}"
+    assert n_out <= allowed, f"{name}: {n_out}/{ratio.size} elements beyond {rtol} (allowed {allowed:.0f}); {where}"
+    assert worst <= worst_allowed, f"{name}: worst element {worst:.3e} > {worst_allowed:.3e}; {where}"
     return worst, normwise

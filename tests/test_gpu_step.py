@@ -85,21 +85,29 @@ def test_mlp_two_streams_equal_one_stream():
 
 # ------------------------------------------------------------------ GPT
 
-def check_adamw_params(got, ref, g_ref, lr, alpha, name):
-    """After an AdamW step from zero moments the local update is
-    -lr * g/(|g| + eps): where the two sides' gradients agree in sign the
-    mixed parameters agree to 1e-5; where the reference gradient is tiny the
-    bf16 gradient may flip its sign, which moves the step by at most
-    2 lr (1 - alpha) -- both results are valid AdamW steps."""
-    got, ref, g_ref = (np.asarray(a, np.float64) for a in (got, ref, g_ref))
-    rms_g = np.sqrt(np.mean(g_ref ** 2)) if g_ref.size else 0.0
-    firm = np.abs(g_ref) > 0.1 * rms_g
-    if firm.any():
-        compare(got[firm], ref[firm], 1e-5, name + " (firm gradient)")
-    loose = ~firm
-    if loose.any():
-        assert np.all(np.abs(got[loose] - ref[loose]) <= 2 * lr * (1 - alpha) * 1.001
-                      + 1e-5 * (np.abs(ref[loose]) + 1e-3)), name
+def check_adamw_params(got, ref, m_gpu, g_ref, cfg, name):
+    """Chained check of the mixed parameters after the first AdamW step from
+    zero moments.  The bias-corrected moments are then m = g and v = g^2, so
+    the local update is u(g) = lr g / (|g| + eps), and two runs whose
+    gradients differ move a parameter apart by (1 - alpha) |u(g_gpu) -
+    u(g_ref)| (up to 2 lr (1 - alpha) where the two gradients differ in
+    sign).  The GPU's gradient is read back from its first moment, m =
+    (1 - beta1) g (for the fused schedule the only place it is kept).  Every
+    element must lie within that distance plus 1e-5 (|ref| + rms(ref)); where
+    the gradients agree, that is the 1e-5 bar of the update itself."""
+    got, ref, m_gpu, g_ref = (np.asarray(a, np.float64) for a in (got, ref, m_gpu, g_ref))
+    if ref.size == 0:
+        return
+    g_gpu = m_gpu / (1.0 - cfg.beta1)
+    u = lambda g: cfg.lr * g / (np.abs(g) + cfg.eps)
+    rms = np.sqrt(np.mean(ref * ref))
+    allow = (1.0 - cfg.alpha) * np.abs(u(g_gpu) - u(g_ref)) + 1e-5 * (np.abs(ref) + rms)
+    bad = np.abs(got - ref) > allow
+    if bad.any():
+        i = np.unravel_index(np.argmax(np.abs(got - ref) - allow), ref.shape)
+        raise AssertionError(f"{name}: {int(bad.sum())}/{bad.size} parameters beyond the update's "
+                             f"propagated bar; worst at {i}: gpu={got[i]!r} ref={ref[i]!r} "
+                             f"g_gpu={g_gpu[i]!r} g_ref={g_ref[i]!r}")
 
 
 @pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48,
@@ -189,7 +197,7 @@ def _step_parity(cfg, schedule):
     got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
     for k in op:
         shp = got_p[k].shape
-        check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
+        check_adamw_params(got_p[k], op[k].reshape(shp), got_m[k], ograds[k].reshape(shp), cfg,
                            f"param {k}")
         compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}", exact=xm[k].reshape(shp))
         compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}", exact=xv[k].reshape(shp))
@@ -285,10 +293,10 @@ def test_gpt_peer_slots_select_replicas():
     ov = {k: np.zeros_like(v) for k, v in op.items()}
     _, ograds, _, _ = O.gpt_step(op, om, ov, {k: v.astype(np.float64) for k, v in peers[2].items()},
                                  tokens, cfg.n_head, ohp, cfg.alpha)
-    got = m.read("params")
+    got, got_m = m.read("params"), m.read("m")
     for k in ["lnf.g", "h1.ln2.b", "h0.qkv.w"]:
-        check_adamw_params(got[k], op[k].reshape(got[k].shape), ograds[k].reshape(got[k].shape),
-                           cfg.lr, cfg.alpha, k)
+        check_adamw_params(got[k], op[k].reshape(got[k].shape), got_m[k], ograds[k].reshape(got[k].shape),
+                           cfg, k)
     m.close()
 
 
@@ -365,7 +373,7 @@ def test_fused_dw_schedule_matches_oracle(cfg):
     got_p, got_m, got_v = m.read("params"), m.read("m"), m.read("v")
     for k in op:
         shp = got_p[k].shape
-        check_adamw_params(got_p[k], op[k].reshape(shp), ograds[k].reshape(shp), cfg.lr, cfg.alpha,
+        check_adamw_params(got_p[k], op[k].reshape(shp), got_m[k], ograds[k].reshape(shp), cfg,
                            f"param {k}")
         compare_chained(got_m[k], om[k].reshape(shp), 2e-2, f"m {k}", exact=xm[k].reshape(shp))
         compare_chained(got_v[k], ov[k].reshape(shp), 4e-2, f"v {k}", exact=xv[k].reshape(shp))
