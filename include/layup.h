@@ -227,6 +227,26 @@ layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors,
                                     const layup_hparams* hp, float alpha, int32_t mix_mode,
                                     float* disagreement, void* stream);
 
+/* layup_layer_update_mix without a context, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same kernels and results, with the
+ * disagreement output (device float, nullable) allowed.  Its per-workgroup
+ * partial sums live in a fixed array of the library in device memory
+ * (16384 floats = 64 KiB per GPU, kept until the process ends).  The
+ * update+mix grid is capped at that many workgroups (larger tensors are
+ * walked in a grid-stride loop), so tensors of any size fit; with a
+ * disagreement output a call takes at most 16 tensors (one launch), more are
+ * refused with LAYUP_ERR_INVALID_ARG.  Nothing is allocated or freed.  Every
+ * call on one GPU shares that GPU's array: calls with a disagreement output
+ * that overlap on one GPU (different streams, or different host threads)
+ * race and may report wrong sums; their tensor updates are unaffected.
+ * Each call writes every partial it reads, so nothing needs clearing
+ * between calls.  stream NULL = the default stream.  Errors are reported
+ * through layup_global_error. */
+layup_status layup_layer_update_mix_static(const layup_tensor* tensors, int32_t n_tensors,
+                                           const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                           float* disagreement, void* stream);
+
 /* Push-mode update of one unit of the model (Algorithm 1 "Local Update",
  * "Communication" and "Peer Update" as written): the worker's own layer gets
  * the local update, then the receiving replica's copy of the layer becomes

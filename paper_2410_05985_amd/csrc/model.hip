@@ -798,6 +798,93 @@ std::string check_push_target(layup_ctx* c, const float* peer, const uint16_t* p
   return "";
 }
 
+// Update+mix of caller-described tensors (layup_layer_update_mix and its
+// allocation-free variant): checks every tensor, then one launch per 16
+// tensors.  part: the disagreement partial sums (one float per workgroup),
+// part_floats of them.
+layup_status tensors_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
+                                const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                float* disagreement, float* part, int64_t part_floats, hipStream_t s) {
+  if (!tensors || n_tensors < 1) return fail(ctx, LAYUP_ERR_INVALID_ARG, "no tensors");
+  if (mix_mode != LAYUP_MIX_PULL && mix_mode != LAYUP_MIX_PUSH)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown mix mode");
+  const bool push = mix_mode == LAYUP_MIX_PUSH;
+  std::string m = check_hp(hp);
+  if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
+  if (disagreement && n_tensors > UM_MAX_TENSORS)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
+  std::vector<UMTensor> ts(n_tensors);
+  for (int i = 0; i < n_tensors; ++i) {
+    const layup_tensor& t = tensors[i];
+    if (t.numel < 0) return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": negative size");
+    if (t.numel == 0) {  // nothing to read or write: the pointers are not used
+      ts[i] = UMTensor{};
+      continue;
+    }
+    if (!t.param || !t.grad || !t.state0 || !t.peer)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": null pointer");
+    if (hp->kind == LAYUP_ADAMW && !t.state1)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": AdamW needs state1");
+    uintptr_t al = (uintptr_t)t.param | (uintptr_t)t.grad | (uintptr_t)t.state0 | (uintptr_t)t.peer |
+                   (uintptr_t)(hp->kind == LAYUP_ADAMW ? t.state1 : nullptr);
+    if (al & 15) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": pointers must be 16-byte aligned");
+    if (((uintptr_t)t.param_bf16 | (uintptr_t)(push ? t.peer_bf16 : nullptr)) & 7)
+      return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": bf16 copies must be 8-byte aligned");
+    if ((const void*)t.param == (const void*)t.peer || (const void*)t.param == (const void*)t.grad)
+      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": param aliases grad or peer");
+    UMTensor& u = ts[i];
+    u.p = t.param;
+    u.g = t.grad;
+    u.m = t.state0;
+    u.v = hp->kind == LAYUP_ADAMW ? t.state1 : nullptr;
+    u.q = t.peer;
+    u.p16 = t.param_bf16;
+    u.q16 = push ? t.peer_bf16 : nullptr;
+    u.n = t.numel;
+    u.decay = t.decay ? 1 : 0;
+    u.pad = 0;
+  }
+  // the launcher caps its grid at UM_MAX_BLOCKS workgroups, one partial each
+  if (disagreement && (!part || part_floats < UM_MAX_BLOCKS))
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "disagreement scratch smaller than the update+mix grid");
+  TraceInfo tr;
+  for (int i = 0; i < n_tensors; i += UM_MAX_TENSORS) {
+    int n = std::min(UM_MAX_TENSORS, n_tensors - i);
+    hipError_t e = launch_update_mix(&ts[i], n, *hp, alpha, disagreement, part, tr, s, push);
+    if (e != hipSuccess) return hip_fail(ctx, e, "update+mix");
+  }
+  return LAYUP_OK;
+}
+
+// Scratch of layup_layer_update_mix_static, for callers that cannot allocate
+// device memory: the disagreement's per-workgroup partial sums.  Each GPU
+// holds its own copy for the life of the process.  In host code the array's
+// name is not a device address: its address on the current device comes from
+// hipGetSymbolAddress, taken once per device and kept.
+constexpr int64_t STATIC_SCRATCH_FLOATS = UM_MAX_BLOCKS;  // 64 KiB
+static __device__ __align__(256) float scratch[STATIC_SCRATCH_FLOATS];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+float* g_scratch_ptr[MAX_DEVICES] = {};
+
+// The current device's address of `scratch`; an error message on failure.
+std::string static_scratch(float** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return std::string("hipGetDevice: ") + hipGetErrorString(e);
+  if (dev < 0 || dev >= MAX_DEVICES) return "device index beyond the scratch table";
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e);
+    g_scratch_ptr[dev] = static_cast<float*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return "";
+}
+
 }  // namespace
 
 // ===================================================================== ABI
@@ -1024,56 +1111,25 @@ layup_status layup_unit_update_push(layup_ctx* ctx, int32_t unit, const layup_hp
 layup_status layup_layer_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
                                     const layup_hparams* hp, float alpha, int32_t mix_mode,
                                     float* disagreement, void* stream) {
-  if (!tensors || n_tensors < 1) return fail(ctx, LAYUP_ERR_INVALID_ARG, "no tensors");
-  if (mix_mode != LAYUP_MIX_PULL && mix_mode != LAYUP_MIX_PUSH)
-    return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown mix mode");
-  const bool push = mix_mode == LAYUP_MIX_PUSH;
-  std::string m = check_hp(hp);
-  if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
   if (disagreement && !ctx)
     return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output needs a context (its partial sums live in the workspace)");
-  std::vector<UMTensor> ts(n_tensors);
-  for (int i = 0; i < n_tensors; ++i) {
-    const layup_tensor& t = tensors[i];
-    if (t.numel < 0) return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": negative size");
-    if (t.numel == 0) {  // nothing to read or write: the pointers are not used
-      ts[i] = UMTensor{};
-      continue;
-    }
-    if (!t.param || !t.grad || !t.state0 || !t.peer)
-      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": null pointer");
-    if (hp->kind == LAYUP_ADAMW && !t.state1)
-      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": AdamW needs state1");
-    uintptr_t al = (uintptr_t)t.param | (uintptr_t)t.grad | (uintptr_t)t.state0 | (uintptr_t)t.peer |
-                   (uintptr_t)(hp->kind == LAYUP_ADAMW ? t.state1 : nullptr);
-    if (al & 15) return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": pointers must be 16-byte aligned");
-    if (((uintptr_t)t.param_bf16 | (uintptr_t)(push ? t.peer_bf16 : nullptr)) & 7)
-      return fail(ctx, LAYUP_ERR_ALIGN, "tensor " + std::to_string(i) + ": bf16 copies must be 8-byte aligned");
-    if ((const void*)t.param == (const void*)t.peer || (const void*)t.param == (const void*)t.grad)
-      return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": param aliases grad or peer");
-    UMTensor& u = ts[i];
-    u.p = t.param;
-    u.g = t.grad;
-    u.m = t.state0;
-    u.v = hp->kind == LAYUP_ADAMW ? t.state1 : nullptr;
-    u.q = t.peer;
-    u.p16 = t.param_bf16;
-    u.q16 = push ? t.peer_bf16 : nullptr;
-    u.n = t.numel;
-    u.decay = t.decay ? 1 : 0;
-    u.pad = 0;
-  }
   hipStream_t s = stream ? (hipStream_t)stream : (ctx ? ctx->su : nullptr);
-  TraceInfo tr;
-  float* part = ctx ? ctx->dis_partial : nullptr;
+  return tensors_update_mix(ctx, tensors, n_tensors, hp, alpha, mix_mode, disagreement,
+                            ctx ? ctx->dis_partial : nullptr, UM_MAX_BLOCKS, s);
+}
+
+layup_status layup_layer_update_mix_static(const layup_tensor* tensors, int32_t n_tensors,
+                                           const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                           float* disagreement, void* stream) {
+  float* part = nullptr;
   if (disagreement && n_tensors > UM_MAX_TENSORS)
-    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
-  for (int i = 0; i < n_tensors; i += UM_MAX_TENSORS) {
-    int n = std::min(UM_MAX_TENSORS, n_tensors - i);
-    hipError_t e = launch_update_mix(&ts[i], n, *hp, alpha, disagreement, part, tr, s, push);
-    if (e != hipSuccess) return hip_fail(ctx, e, "update+mix");
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
+  if (disagreement && tensors && n_tensors >= 1) {
+    std::string m = static_scratch(&part);
+    if (!m.empty()) return fail(nullptr, LAYUP_ERR_HIP, m);
   }
-  return LAYUP_OK;
+  return tensors_update_mix(nullptr, tensors, n_tensors, hp, alpha, mix_mode, disagreement, part,
+                            STATIC_SCRATCH_FLOATS, (hipStream_t)stream);
 }
 
 layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* a) {
