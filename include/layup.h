@@ -247,6 +247,29 @@ layup_status layup_layer_update_mix_static(const layup_tensor* tensors, int32_t 
                                            const layup_hparams* hp, float alpha, int32_t mix_mode,
                                            float* disagreement, void* stream);
 
+/* Update+mix of several units whose gradients are all ready (Algorithm 1's
+ * updater taking the layers in backward order: "Local Update" and "Peer
+ * Update" of each), in as few passes as possible.  tensors are listed unit by
+ * unit in the order the units are visited (output side first); units[i]
+ * (host array) is tensor i's unit id, 0 <= id < 2^30, and a unit's tensors
+ * are adjacent (a unit id that reappears after another unit is
+ * LAYUP_ERR_INVALID_ARG).  When every non-empty tensor sits at the same place
+ * in the param, grad, state and peer buffers (the same byte distance from
+ * param to grad, state0, state1 and peer for each tensor, bf16 copies at the
+ * param's element offset: a flat layout such as layup_tensor_layout's) and
+ * the tensors span fewer than 2^31 elements, up to 192 tensors of whole units
+ * go in one launch, their chunks numbered unit by unit in list order;
+ * otherwise each unit is its own launch (as layup_layer_update_mix).  The
+ * result is the same either way.  trace (device, nullable; trace_counter
+ * required with it) receives one (trace_step, unit) pair per unit in list
+ * order.  No disagreement output.  stream NULL = the default stream; no
+ * context; errors through layup_global_error.  Tensor rules as
+ * layup_tensor. */
+layup_status layup_units_update_mix(const layup_tensor* tensors, const int32_t* units, int32_t n_tensors,
+                                    const layup_hparams* hp, float alpha, int32_t mix_mode, int32_t* trace,
+                                    int32_t* trace_counter, int32_t trace_capacity, int32_t trace_step,
+                                    void* stream);
+
 /* Push-mode update of one unit of the model (Algorithm 1 "Local Update",
  * "Communication" and "Peer Update" as written): the worker's own layer gets
  * the local update, then the receiving replica's copy of the layer becomes

@@ -43,6 +43,15 @@ hipError_t launch_update_mix(const UMTensor* ts, int n, const layup_hparams& hp,
                              float* dis_out, float* dis_partial, const TraceInfo& tr,
                              hipStream_t stream, bool push = false);
 
+// Several units whose gradients are all ready, in one launch: up to
+// UMF_MAX_TENSORS tensors that share one flat layout (update_mix_flat_layout),
+// listed unit by unit in the order the units are visited; units[i] is tensor
+// i's unit.  One trace entry per unit (tr.unit unused).  No disagreement.
+constexpr int UMF_MAX_TENSORS = 192;
+bool update_mix_flat_layout(const UMTensor* ts, int n, bool adamw, bool push, int* base_index);
+hipError_t launch_update_mix_flat(const UMTensor* ts, const int32_t* units, int n, const layup_hparams& hp,
+                                  float alpha, const TraceInfo& tr, hipStream_t stream, bool push);
+
 // ------------------------------------------------------------------ GEMM
 enum Epilogue : int {
   EPI_F32 = 0,    // C(f32) = acc + bias (+ aux residual f32)

@@ -802,18 +802,16 @@ std::string check_push_target(layup_ctx* c, const float* peer, const uint16_t* p
 // allocation-free variant): checks every tensor, then one launch per 16
 // tensors.  part: the disagreement partial sums (one float per workgroup),
 // part_floats of them.
-layup_status tensors_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
-                                const layup_hparams* hp, float alpha, int32_t mix_mode,
-                                float* disagreement, float* part, int64_t part_floats, hipStream_t s) {
+// Checks caller-described tensors and converts them to kernel descriptors.
+layup_status collect_tensors(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
+                             const layup_hparams* hp, int32_t mix_mode, std::vector<UMTensor>& ts) {
   if (!tensors || n_tensors < 1) return fail(ctx, LAYUP_ERR_INVALID_ARG, "no tensors");
   if (mix_mode != LAYUP_MIX_PULL && mix_mode != LAYUP_MIX_PUSH)
     return fail(ctx, LAYUP_ERR_INVALID_ARG, "unknown mix mode");
   const bool push = mix_mode == LAYUP_MIX_PUSH;
   std::string m = check_hp(hp);
   if (!m.empty()) return fail(ctx, LAYUP_ERR_INVALID_ARG, m);
-  if (disagreement && n_tensors > UM_MAX_TENSORS)
-    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
-  std::vector<UMTensor> ts(n_tensors);
+  ts.assign(n_tensors, UMTensor{});
   for (int i = 0; i < n_tensors; ++i) {
     const layup_tensor& t = tensors[i];
     if (t.numel < 0) return fail(ctx, LAYUP_ERR_INVALID_ARG, "tensor " + std::to_string(i) + ": negative size");
@@ -844,6 +842,17 @@ layup_status tensors_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int
     u.decay = t.decay ? 1 : 0;
     u.pad = 0;
   }
+  return LAYUP_OK;
+}
+
+layup_status tensors_update_mix(layup_ctx* ctx, const layup_tensor* tensors, int32_t n_tensors,
+                                const layup_hparams* hp, float alpha, int32_t mix_mode,
+                                float* disagreement, float* part, int64_t part_floats, hipStream_t s) {
+  std::vector<UMTensor> ts;
+  TRY(collect_tensors(ctx, tensors, n_tensors, hp, mix_mode, ts));
+  const bool push = mix_mode == LAYUP_MIX_PUSH;
+  if (disagreement && n_tensors > UM_MAX_TENSORS)
+    return fail(ctx, LAYUP_ERR_INVALID_ARG, "the disagreement output supports at most 16 tensors per call");
   // the launcher caps its grid at UM_MAX_BLOCKS workgroups, one partial each
   if (disagreement && (!part || part_floats < UM_MAX_BLOCKS))
     return fail(ctx, LAYUP_ERR_INVALID_ARG, "disagreement scratch smaller than the update+mix grid");
@@ -1130,6 +1139,67 @@ layup_status layup_layer_update_mix_static(const layup_tensor* tensors, int32_t 
   }
   return tensors_update_mix(nullptr, tensors, n_tensors, hp, alpha, mix_mode, disagreement, part,
                             STATIC_SCRATCH_FLOATS, (hipStream_t)stream);
+}
+
+layup_status layup_units_update_mix(const layup_tensor* tensors, const int32_t* units, int32_t n_tensors,
+                                    const layup_hparams* hp, float alpha, int32_t mix_mode, int32_t* trace,
+                                    int32_t* trace_counter, int32_t trace_capacity, int32_t trace_step,
+                                    void* stream) {
+  std::vector<UMTensor> ts;
+  TRY(collect_tensors(nullptr, tensors, n_tensors, hp, mix_mode, ts));
+  if (!units) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "null unit list");
+  if (trace && (!trace_counter || trace_capacity < 1))
+    return fail(nullptr, LAYUP_ERR_INVALID_ARG, "trace needs a counter and a positive capacity");
+  // a unit's tensors are adjacent: a unit id that reappears after another unit is refused
+  std::vector<int32_t> seen;
+  for (int i = 0; i < n_tensors; ++i) {
+    if (units[i] < 0 || units[i] >= (1 << 30)) return fail(nullptr, LAYUP_ERR_INVALID_ARG, "unit id out of range");
+    if (i > 0 && units[i] == units[i - 1]) continue;
+    if (std::find(seen.begin(), seen.end(), units[i]) != seen.end())
+      return fail(nullptr, LAYUP_ERR_INVALID_ARG, "the tensors of a unit must be adjacent");
+    seen.push_back(units[i]);
+  }
+  const bool push = mix_mode == LAYUP_MIX_PUSH;
+  const hipStream_t s = (hipStream_t)stream;
+  TraceInfo tr;
+  tr.trace = trace;
+  tr.counter = trace_counter;
+  tr.capacity = trace_capacity;
+  tr.step = trace_step;
+  int dummy = 0;
+  const bool flat = update_mix_flat_layout(ts.data(), n_tensors, hp->kind == LAYUP_ADAMW, push, &dummy);
+  // whole units, in order, grouped into launches of up to UMF_MAX_TENSORS
+  // tensors (flat layout), else one unit at a time
+  int i = 0;
+  while (i < n_tensors) {
+    int j = i;  // end of the group
+    while (j < n_tensors) {
+      int k = j + 1;
+      while (k < n_tensors && units[k] == units[j]) ++k;  // end of unit at j
+      if (flat && k - i <= UMF_MAX_TENSORS) {
+        j = k;
+        continue;
+      }
+      if (j == i) j = k;  // a unit alone
+      break;
+    }
+    hipError_t e;
+    if (flat && j - i <= UMF_MAX_TENSORS) {
+      e = launch_update_mix_flat(&ts[i], units + i, j - i, *hp, alpha, tr, s, push);
+    } else {
+      // one unit: launches of up to 16 tensors, the trace entry with the first
+      e = hipSuccess;
+      for (int a = i; a < j && e == hipSuccess; a += UM_MAX_TENSORS) {
+        TraceInfo t2 = tr;
+        t2.unit = units[i];
+        if (a > i) t2.trace = nullptr;
+        e = launch_update_mix(&ts[a], std::min(UM_MAX_TENSORS, j - a), *hp, alpha, nullptr, nullptr, t2, s, push);
+      }
+    }
+    if (e != hipSuccess) return hip_fail(nullptr, e, "update+mix of several units");
+    i = j;
+  }
+  return LAYUP_OK;
 }
 
 layup_status layup_step_ex(layup_ctx* ctx, const layup_step_args* a) {

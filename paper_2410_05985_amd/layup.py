@@ -86,7 +86,8 @@ EXPORTS = [
     "layup_param_layout", "layup_tensor_layout", "layup_workspace_size", "layup_init",
     "layup_destroy", "layup_last_error", "layup_global_error", "layup_synchronize",
     "layup_refresh_shadow", "layup_forward", "layup_layer_backward", "layup_unit_update_mix",
-    "layup_layer_update_mix", "layup_layer_update_mix_static", "layup_unit_update_push", "layup_step_ex", "layup_step",
+    "layup_layer_update_mix", "layup_layer_update_mix_static", "layup_units_update_mix",
+    "layup_unit_update_push", "layup_step_ex", "layup_step",
     "layup_unit_timeline", "layup_gemm_timing", "layup_gemm_timing_read", "layup_push_sum_send", "layup_push_sum_receive", "layup_activation",
     "layup_gemm_bf16", "layup_gemm_f32",
 ]
@@ -119,6 +120,8 @@ def lib() -> C.CDLL:
         "layup_unit_update_mix": ([P, C.c_int32, P, C.c_float, C.c_int32, P], C.c_int),
         "layup_layer_update_mix": ([P, P, C.c_int32, P, C.c_float, C.c_int32, P, P], C.c_int),
         "layup_layer_update_mix_static": ([P, C.c_int32, P, C.c_float, C.c_int32, P, P], C.c_int),
+        "layup_units_update_mix": ([P, P, C.c_int32, P, C.c_float, C.c_int32, P, P, C.c_int32, C.c_int32, P],
+                                   C.c_int),
         "layup_unit_update_push": ([P, C.c_int32, P, C.c_float, P, P, P], C.c_int),
         "layup_step_ex": ([P, P], C.c_int),
         "layup_step": ([P, P, P, P, C.c_float, C.c_int32, P, P], C.c_int),
@@ -266,6 +269,15 @@ def layup_layer_update_mix_static(tensors: List[layup_tensor], hp: layup_hparams
     arr = (layup_tensor * len(tensors))(*tensors)
     _check(lib().layup_layer_update_mix_static(arr, len(tensors), C.byref(hp), alpha, mix_mode,
                                                _ptr(disagreement), _stream(stream)))
+
+
+def layup_units_update_mix(tensors: List[layup_tensor], units: List[int], hp: layup_hparams, alpha: float,
+                           mix_mode: int = LAYUP_MIX_PULL, trace=None, trace_counter=None,
+                           trace_capacity: int = 0, trace_step: int = 0, stream=None):
+    arr = (layup_tensor * len(tensors))(*tensors)
+    uarr = (C.c_int32 * len(units))(*units)
+    _check(lib().layup_units_update_mix(arr, uarr, len(tensors), C.byref(hp), alpha, mix_mode, _ptr(trace),
+                                        _ptr(trace_counter), trace_capacity, trace_step, _stream(stream)))
 
 
 def layup_unit_update_push(ctx, unit: int, hp: layup_hparams, alpha: float, peer_params,

@@ -207,3 +207,168 @@ def test_update_mix_resnet50_sweep_full_size():
         compare(dev[n]["p"].cpu().numpy(), ref_p, 1e-5, f"p {n}")
         compare(dev[n]["m"].cpu().numpy(), ref_m, 1e-5, f"m {n}")
 
+
+
+# --------------------------------------------- several ready units, one pass
+
+def _flat(arrays, sizes, pad=64):
+    """Device buffers holding the given per-tensor arrays back to back (each
+    offset a multiple of `pad` elements); returns the buffers and offsets."""
+    offs, o = [], 0
+    for n in sizes:
+        offs.append(o)
+        o += (n + pad - 1) // pad * pad
+    bufs = {}
+    for key, arrs in arrays.items():
+        host = np.zeros(max(o, 1), np.float32)
+        for off, a in zip(offs, arrs):
+            if a is not None:
+                host[off: off + a.size] = a.reshape(-1)
+        bufs[key] = _dev(host)
+    return bufs, offs
+
+
+def _descs_flat(bufs, offs, sizes, decays, with_v=False, p16=None, q16=None):
+    out = []
+    for off, n, dec in zip(offs, sizes, decays):
+        a = 4 * off
+        out.append(LU.layup_tensor(param=bufs["p"].data_ptr() + a, grad=bufs["g"].data_ptr() + a,
+                                   state0=bufs["m"].data_ptr() + a,
+                                   state1=bufs["v"].data_ptr() + a if with_v else None,
+                                   peer=bufs["q"].data_ptr() + a,
+                                   param_bf16=p16.data_ptr() + 2 * off if p16 is not None else None,
+                                   peer_bf16=q16.data_ptr() + 2 * off if q16 is not None else None,
+                                   numel=n, decay=int(dec)))
+    return out
+
+
+def test_units_update_mix_resnet50_one_pass():
+    """The whole ResNet-50 sweep (54 units, 161 tensors, flat buffers) in one
+    call of layup_units_update_mix: every tensor against the oracle at rel
+    1e-5, one trace entry per unit in reverse unit order."""
+    params, grads, peer = S.resnet50_tensors()
+    units = S.resnet50_units()
+    names = [n for u in reversed(units) for n in u]
+    unit_of = [len(units) - 1 - i for i, u in enumerate(reversed(units)) for _ in u]
+    sizes = [params[n].size for n in names]
+    bufs, offs = _flat({"p": [params[n] for n in names], "g": [grads[n] for n in names],
+                        "m": [None] * len(names), "q": [peer[n] for n in names]}, sizes)
+    kw = dict(lr=0.1, momentum=0.9, weight_decay=5e-5)
+    trace = torch.zeros(2 * 64, dtype=torch.int32, device=DEV)
+    counter = torch.zeros(1, dtype=torch.int32, device=DEV)
+    torch.cuda.synchronize()
+    LU.layup_units_update_mix(_descs_flat(bufs, offs, sizes, [1] * len(names)), unit_of, _hp("sgd", 1, **kw),
+                              0.5, trace=trace, trace_counter=counter, trace_capacity=64, trace_step=7,
+                              stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert counter.item() == 54
+    tr = trace[:108].cpu().numpy().reshape(-1, 2)
+    assert [tuple(r) for r in tr] == [(7, u) for u in range(53, -1, -1)]
+    p_all, m_all = bufs["p"].cpu().numpy(), bufs["m"].cpu().numpy()
+    for n, off, sz in zip(names, offs, sizes):
+        p = params[n].reshape(-1)
+        ref_p, ref_m, _, _ = O.update_mix(p, grads[n].reshape(-1), np.zeros_like(p), None,
+                                          peer[n].reshape(-1), _ohp("sgd", **kw), 0.5, 1)
+        compare(p_all[off: off + sz], ref_p, 1e-5, f"p {n}")
+        compare(m_all[off: off + sz], ref_m, 1e-5, f"m {n}")
+
+
+@pytest.mark.parametrize("push", [False, True], ids=["pull", "push"])
+def test_units_update_mix_equals_per_unit_launches(push):
+    """AdamW with bf16 copies, ragged and empty tensors, 230 tensors in 80
+    units (two passes of whole units, the second shorter): one call of
+    layup_units_update_mix on flat buffers gives bit for bit what one
+    layup_layer_update_mix call per unit gives, in both mixing forms; a
+    table that is not flat (each tensor its own allocation) takes the
+    per-unit path with the same results and trace."""
+    rng = np.random.default_rng(21)
+    n_units = 80
+    unit_sizes = [3 if u % 3 else 2 for u in range(n_units)]
+    unit_of = [u for u in range(n_units - 1, -1, -1) for _ in range(unit_sizes[u])]
+    sizes = [int(rng.choice([0, 1, 3, 5, 64, 257, 2048, 3001, 40000])) for _ in unit_of]
+    decays = [int(i % 2) for i in range(len(sizes))]
+    inputs = [S.update_mix_inputs(max(n, 1), 500 + i, "adamw") for i, n in enumerate(sizes)]
+    arrays = {k: [inp[j][: n] for inp, n in zip(inputs, sizes)] for j, k in enumerate("pgmvq")}
+    hp = _hp("adamw", 4)
+    results = []
+    for mode in ("units", "per-unit", "not-flat"):
+        if mode == "not-flat":
+            dev = [{k: _dev(np.concatenate([arrays[k][i], np.zeros(1, np.float32)])) for k in "pgmvq"}
+                   for i in range(len(sizes))]
+            p16s = [torch.zeros(n + 1, dtype=torch.int16, device=DEV) for n in sizes]
+            q16s = [torch.zeros(n + 1, dtype=torch.int16, device=DEV) for n in sizes]
+            descs = [LU.layup_tensor(param=d["p"].data_ptr(), grad=d["g"].data_ptr(), state0=d["m"].data_ptr(),
+                                     state1=d["v"].data_ptr(), peer=d["q"].data_ptr(),
+                                     param_bf16=a.data_ptr(), peer_bf16=b.data_ptr() if push else None,
+                                     numel=n, decay=dec)
+                     for d, a, b, n, dec in zip(dev, p16s, q16s, sizes, decays)]
+        else:
+            bufs, offs = _flat(arrays, sizes)
+            tot = bufs["p"].numel()
+            p16 = torch.zeros(tot, dtype=torch.int16, device=DEV)
+            q16 = torch.zeros(tot, dtype=torch.int16, device=DEV)
+            descs = _descs_flat(bufs, offs, sizes, decays, with_v=True, p16=p16, q16=q16 if push else None)
+        trace = torch.zeros(2 * 128, dtype=torch.int32, device=DEV)
+        counter = torch.zeros(1, dtype=torch.int32, device=DEV)
+        mix = LU.LAYUP_MIX_PUSH if push else LU.LAYUP_MIX_PULL
+        torch.cuda.synchronize()
+        if mode == "per-unit":
+            i = 0
+            while i < len(descs):
+                j = i
+                while j < len(descs) and unit_of[j] == unit_of[i]:
+                    j += 1
+                LU.layup_layer_update_mix(None, descs[i:j], hp, 0.3, stream=torch.cuda.current_stream(),
+                                          mix_mode=mix)
+                i = j
+        else:
+            LU.layup_units_update_mix(descs, unit_of, hp, 0.3, mix_mode=mix, trace=trace, trace_counter=counter,
+                                      trace_capacity=128, trace_step=2, stream=torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        if mode != "per-unit":
+            assert counter.item() == n_units
+            tr = trace[: 2 * n_units].cpu().numpy().reshape(-1, 2)
+            assert [tuple(r) for r in tr] == [(2, u) for u in range(n_units - 1, -1, -1)]
+        per_tensor = []
+        for i, n in enumerate(sizes):
+            if mode == "not-flat":
+                d = dev[i]
+                vals = [d[k][:n].cpu().numpy() for k in "pmvq"] + [p16s[i][:n].cpu().numpy(),
+                                                                      q16s[i][:n].cpu().numpy()]
+            else:
+                o = offs[i]
+                vals = [bufs[k][o: o + n].cpu().numpy() for k in "pmvq"] + [p16[o: o + n].cpu().numpy(),
+                                                                           q16[o: o + n].cpu().numpy()]
+            per_tensor.append(vals)
+        results.append(per_tensor)
+    for other in results[1:]:
+        for a, b in zip(results[0], other):
+            for x, y in zip(a, b):
+                assert np.array_equal(x, y)
+    # and the oracle, on the parameters
+    for i, n in enumerate(sizes):
+        if n == 0:
+            continue
+        p, g, m, v, q = (arrays[k][i] for k in "pgmvq")
+        if push:
+            rp, rm, rv, rq, _ = O.update_push(p, g, m, v, q, _ohp("adamw"), 0.3, 4, wd_on=bool(decays[i]))
+            compare(results[0][i][3], rq, 1e-5, f"q {i}")
+        else:
+            rp, rm, rv, _ = O.update_mix(p, g, m, v, q, _ohp("adamw"), 0.3, 4, wd_on=bool(decays[i]))
+        compare(results[0][i][0], rp, 1e-5, f"p {i}")
+
+
+def test_units_update_mix_argument_checks():
+    """A unit whose tensors are not adjacent, a missing unit list, or a trace
+    without its counter is refused before any work is enqueued."""
+    bufs, offs = _flat({k: [np.ones(8, np.float32)] * 3 for k in "pgmq"}, [8, 8, 8])
+    descs = _descs_flat(bufs, offs, [8, 8, 8], [1, 1, 1])
+    hp = _hp("sgd")
+    with pytest.raises(LU.LayupError):
+        LU.layup_units_update_mix(descs, [2, 1, 2], hp, 0.5)
+    st = LU.lib().layup_units_update_mix((LU.layup_tensor * 3)(*descs), None, 3, LU.C.byref(hp), 0.5, 0,
+                                         None, None, 0, 0, None)
+    assert st == LU.LAYUP_ERR_INVALID_ARG
+    trace = torch.zeros(8, dtype=torch.int32, device=DEV)
+    with pytest.raises(LU.LayupError):
+        LU.layup_units_update_mix(descs, [2, 1, 0], hp, 0.5, trace=trace, trace_capacity=4)
