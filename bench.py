@@ -61,6 +61,15 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--serialize", action="store_true", help="update on the compute stream")
+    ap.add_argument("--only-step", action="store_true",
+                    help="time the layer-wise steps only (for kernel traces of the step)")
+    ap.add_argument("--pmc-summary", nargs=2, default=None, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU run: turn the FETCH_SIZE and WRITE_SIZE counter collections of "
+                         "`rocprofv3 --pmc ... -- python3 bench.py --workload kernels` into "
+                         "profiles/pmc_traffic.json (copy-calibrated bytes per dispatch group)")
+    ap.add_argument("--trace-overlap", default=None, metavar="CSV",
+                    help="no GPU run: read a rocprofv3 kernel trace of --only-step and report how much of "
+                         "the update stream's kernel time ran concurrently with compute-stream kernels")
     ap.add_argument("--workload", default="gpt2-small",
                     choices=["gpt2-small", "gpt2-medium", "gpt-1.3b", "resnet50-update", "mlp",
                              "gossip", "kernels", "gemm-yardstick"])
@@ -175,37 +184,69 @@ def percentiles(xs):
     return dict(p10=round(pick(0.1), 4), median=round(pick(0.5), 4), p90=round(pick(0.9), 4))
 
 
+def host_cpu():
+    """Cores this process may run on and the CPU model (from /proc/cpuinfo)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return n, model
+
+
 def cpu_baseline(cfg_full):
     """The oracle on the host cores: one whole layer-wise step of a stack with
     the full width, sequence length and vocabulary but 1 block and 2 of the 8
     sequences, scaled to the full step by the ratio of the two steps' GEMM
-    FLOPs (the oracle's time is dominated by its float64 matrix products)."""
+    FLOPs (the oracle's time is dominated by its float64 matrix products).
+    Timed twice on the same sample: with every thread the BLAS library uses
+    (the reported value) and with one thread."""
     import threadpoolctl
     import oracle as O
     from paper_2410_05985_amd import synthetic as S
     cfg1 = S.GPTConfig(n_layer=1, d_model=cfg_full.d_model, n_head=cfg_full.n_head,
                        d_ff=cfg_full.d_ff, seq=cfg_full.seq, batch=2,
                        vocab=cfg_full.vocab)
-    params = {k: v.astype(np.float64) for k, v in S.gpt_params(cfg1).items()}
+    params0 = {k: v.astype(np.float64) for k, v in S.gpt_params(cfg1).items()}
     peer = {k: v.astype(np.float64) for k, v in S.gpt_peer(cfg1, S.gpt_params(cfg1)).items()}
     tokens = S.gpt_tokens(cfg1)
-    m = {k: np.zeros_like(v) for k, v in params.items()}
-    v = {k: np.zeros_like(v_) for k, v_ in params.items()}
     hp = dict(optim="adamw", lr=cfg1.lr, weight_decay=cfg1.weight_decay, beta1=cfg1.beta1,
               beta2=cfg1.beta2, eps=cfg1.eps)
+
+    def one_step():
+        params = {k: a.copy() for k, a in params0.items()}
+        m = {k: np.zeros_like(a) for k, a in params.items()}
+        v = {k: np.zeros_like(a) for k, a in params.items()}
+        t0 = time.perf_counter()
+        O.gpt_step(params, m, v, peer, tokens, cfg1.n_head, hp, cfg1.alpha)
+        return time.perf_counter() - t0
+
     threads = max((p.get("num_threads", 1) for p in threadpoolctl.threadpool_info()), default=1)
-    t0 = time.perf_counter()
-    O.gpt_step(params, m, v, peer, tokens, cfg1.n_head, hp, cfg1.alpha)
-    dt = time.perf_counter() - t0
+    dt = one_step()
+    with threadpoolctl.threadpool_limits(limits=1):
+        dt1 = one_step()
 
     def flops(c):
         n, d, f, V = c.batch * c.seq, c.d_model, c.d_ff, c.vocab
         blk = 2 * n * (3 * d * d + d * d + 2 * d * f) * 3 + 4 * c.batch * c.seq * c.seq * d * 3
         return c.n_layer * blk + 2 * n * d * V * 3
     scale = flops(cfg_full) / flops(cfg1)
+    nproc, model = host_cpu()
     return dict(value=dt * scale * 1e3, unit="ms/step", cores=int(threads), kind="oracle",
                 sample=f"one oracle step of a 1-block, batch-2 stack at full width/seq/vocab "
-                       f"({dt:.1f} s), scaled by GEMM FLOPs x{scale:.2f} to 12 blocks x batch 8")
+                       f"({dt:.1f} s with {threads} threads, {dt1:.1f} s with 1), scaled by GEMM FLOPs "
+                       f"x{scale:.2f} to 12 blocks x batch 8",
+                one_thread_ms_per_step=round(dt1 * scale * 1e3, 1),
+                sample_s={"all_threads": round(dt, 3), "one_thread": round(dt1, 3)},
+                host={"nproc": nproc, "cpu_model": model})
 
 
 def gpt_model_on_device(torch, LU, S, cfg, n_peers):
@@ -569,8 +610,131 @@ def bench_kernels(args, torch, LU, S):
                       "update_mix_algorithmic_bytes": 34 * n}), flush=True)
 
 
+def pmc_summary(fetch_csv, write_csv):
+    """HBM bytes of the kernels of `bench.py --workload kernels` from two
+    counter passes.  The 1 GiB device copy calibrates the counters (it reads
+    and writes 1 GiB): fetch and write counts are scaled so that the copy
+    reads and writes exactly that.  The dispatches after the copy are the 8
+    backward GEMMs of a GPT-2-small block (each with its split-K reduction,
+    if any), then the block's update+mix."""
+    import csv
+
+    def load(path, counter):
+        rows = {}
+        with open(path, newline="") as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] != counter:
+                    continue
+                d = int(r["Dispatch_Id"])
+                rows.setdefault(d, [r["Kernel_Name"], 0.0])[1] += float(r["Counter_Value"])
+        return [rows[k] for k in sorted(rows)]
+
+    f, w = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    assert [a[0] for a in f] == [a[0] for a in w], "the two passes ran different dispatches"
+    names = [a[0] for a in f]
+    ci = next(i for i, n in enumerate(names) if "copyBuffer" in n)
+    gib = float(1 << 30)
+    ff, wf = gib / (f[ci][1] * 1024), gib / (w[ci][1] * 1024)
+    gemm_names = ["qkv.dX", "qkv.dW", "proj.dX", "proj.dW", "fc.dX", "fc.dW", "mproj.dX", "mproj.dW"]
+    groups, um = [], None
+    for i in range(ci + 1, len(names)):
+        if "gemm_bf16_kernel" in names[i]:
+            groups.append([i])
+        elif "splitk_reduce" in names[i]:
+            groups[-1].append(i)
+        elif "update_mix_kernel" in names[i]:
+            um = i
+            break
+    assert len(groups) == 8 and um is not None, [names[g[0]][:40] for g in groups]
+    sha = lambda src: hashlib.sha256(open(os.path.join(ROOT, "paper_2410_05985_amd", "csrc", src), "rb")
+                                     .read()).hexdigest()[:16]
+    per, tot = [], 0.0
+    for nm, g in zip(gemm_names, groups):
+        fb = sum(f[i][1] for i in g) * 1024 * ff
+        wb = sum(w[i][1] for i in g) * 1024 * wf
+        tot += fb + wb
+        per.append(dict(gemm=nm, dispatches=len(g), fetch_bytes=fb, write_bytes=wb))
+    ufb, uwb = f[um][1] * 1024 * ff, w[um][1] * 1024 * wf
+    out = dict(fetch_factor=ff, write_factor=wf,
+               gemm_block_backward=dict(source_sha256_16=sha("gemm_bf16.hip"), hbm_bytes=tot, per_gemm=per),
+               update_mix_block=dict(source_sha256_16=sha("update_mix.hip"), hbm_bytes=ufb + uwb,
+                                     fetch_bytes=ufb, write_bytes=uwb, algorithmic_bytes=34 * 7_087_872))
+    with open(os.path.join(ROOT, "profiles", "pmc_traffic.json"), "w") as fo:
+        json.dump(out, fo, indent=1)
+    print(json.dumps({"fetch_factor": ff, "write_factor": wf, "gemm_block_backward_bytes": tot,
+                      "per_gemm": per, "update_mix_block_bytes": ufb + uwb}), flush=True)
+
+
+def trace_overlap(path):
+    """Concurrency of the two streams in a rocprofv3 kernel trace (CSV) of
+    `bench.py --only-step`: the compute stream is the one that runs the
+    attention backward, the update stream the one that runs the update+mix.
+    For the update+mix kernels, and for every kernel of the update stream
+    (dW GEMMs, the head's dW, the forward's second half, the token sort),
+    the fraction of their summed duration during which at least one
+    compute-stream kernel was running, over every step in the trace
+    (warm-up and timed steps are the same step)."""
+    import csv
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append((r["Kernel_Name"], r["Stream_Id"], int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    from collections import Counter
+    um_streams = Counter(sid for n, sid, _, _ in rows if "update_mix_kernel" in n)
+    at_streams = Counter(sid for n, sid, _, _ in rows if "attn_bwd_dq_kernel" in n)
+    comp_c = [k for k in at_streams if k not in um_streams]
+    upd_c = [k for k in um_streams if k not in at_streams]
+    if len(comp_c) != 1 or len(upd_c) != 1:
+        raise SystemExit(f"expected the trace of one two-stream model (bench.py --only-step): compute-stream "
+                         f"candidates {comp_c}, update-stream candidates {upd_c}")
+    comp, upd = comp_c[0], upd_c[0]
+    cint = sorted((a, b) for n, sid, a, b in rows if sid == comp)
+    merged = []
+    for a, b in cint:
+        if merged and a <= merged[-1][1]:
+            merged[-1][1] = max(merged[-1][1], b)
+        else:
+            merged.append([a, b])
+    import bisect
+    starts = [m[0] for m in merged]
+
+    def covered(a, b):
+        i = max(0, bisect.bisect_right(starts, a) - 1)
+        tot = 0
+        while i < len(merged) and merged[i][0] < b:
+            tot += max(0, min(b, merged[i][1]) - max(a, merged[i][0]))
+            i += 1
+        return tot
+
+    def stats(ks):
+        dur = sum(b - a for a, b in ks)
+        conc = sum(covered(a, b) for a, b in ks)
+        return dict(kernels=len(ks), ms_per_step=round(dur * 1e-6 / n_steps, 4),
+                    concurrent_ms_per_step=round(conc * 1e-6 / n_steps, 4),
+                    concurrent_frac=round(conc / max(dur, 1), 4))
+
+    # each step launches the 14 units' update+mix in reverse order: the
+    # 14th of a step is the embeddings' unit, whose gradient is the step's
+    # last (nothing is left on the compute stream to overlap it with)
+    um = sorted((a, b) for n, sid, a, b in rows if sid == upd and "update_mix_kernel" in n)
+    n_steps = max(1, len(um) // 14)
+    out = {"trace": os.path.basename(path), "steps": n_steps,
+           "update_mix": stats(um),
+           "update_mix_blocks_and_final_ln": stats([k for i, k in enumerate(um) if i % 14 != 13]),
+           "update_mix_embeddings": stats([k for i, k in enumerate(um) if i % 14 == 13]),
+           "update_stream_all": stats([(a, b) for n, sid, a, b in rows if sid == upd]),
+           "compute_stream_busy_ms_per_step": round(sum(b - a for a, b in merged) * 1e-6 / n_steps, 4)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
+    if args.trace_overlap:
+        trace_overlap(args.trace_overlap)
+        return
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark runs on one GPU: the layer-wise step of one worker; "
                                    "multi-GPU runs are not part of it", "n_gpus": args.gpus}))
@@ -629,6 +793,12 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     step_ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(args.steps)]
     loss_v = float(loss.item())
+    if args.only_step:
+        print(json.dumps({"metric": "ms per layer-wise step (GPT-2-small), steps only", "value": round(ms_step, 4),
+                          "unit": "ms/step", "steps": args.steps, "warmup": args.warmup,
+                          "step_ms_events": percentiles(step_ms), "loss": round(loss_v, 5),
+                          "streams": 1 if args.serialize else 2}), flush=True)
+        return
 
     # drift (section 3.2): delay from each unit's gradient to its applied
     # update, layer-wise (the last timed step) against one step with every
@@ -706,10 +876,10 @@ def main():
     gemm_tflops = blk_flops / (blk_ms * 1e-3) / 1e12
     um = time_update_mix(torch, LU, model, range(1, cfg.n_layer + 1), hp, cfg.alpha, args.kernel_reps, ks)
     um_all = time_update_mix(torch, LU, model, range(model.n_units), hp, cfg.alpha, args.kernel_reps, ks)
-    overlap = (serial_ms - ms_step) / um_all["round_ms"]
+    moved = serial_ms - ms_step
     print(f"[bench] step events p10/median/p90 {percentiles(step_ms)}; forward {fwd_ms:.3f} ms; "
           f"serialized {serial_ms:.3f} ms; fused dW {fused_ms:.3f} ms; update+mix of all {model.n_units} units {um_all['round_ms']:.3f} ms; "
-          f"overlap {overlap:.2f}", file=sys.stderr, flush=True)
+          f"critical path moved {moved:.3f} ms", file=sys.stderr, flush=True)
     for x in g:
         print(f"[bench] gemm {x['name']:9s} {x['M']}x{x['N']}x{x['K']}: {x['ms']*1e3:8.1f} us "
               f"{x['tflops']:7.1f} TFLOP/s", file=sys.stderr, flush=True)
@@ -756,7 +926,11 @@ def main():
         "serialized_ms_per_step": round(serial_ms, 4),
         "fused_dw_ms_per_step": round(fused_ms, 4),
         "update_mix_all_units_ms": round(um_all["round_ms"], 4),
-        "overlap": round(overlap, 3),
+        "critical_path_moved_ms": round(moved, 4),
+        "moved_off_compute_stream": "serialized minus two-stream step time; the update stream takes the "
+                                    "update+mix of every unit, every dW GEMM with its bias sum, the head's dW, "
+                                    "the forward's second batch half and the token sort (the concurrency of "
+                                    "the update+mix itself comes from a kernel trace: bench.py --trace-overlap)",
         "drift": drift,
         "roofline": roofline,
     }
