@@ -250,6 +250,34 @@ def test_gpt_two_streams_equal_one_stream_and_repeatable(cfg):
             assert torch.equal(a, b), (run, name)
 
 
+def test_gpt_repeated_and_out_of_vocabulary_tokens_two_streams_equal_one_stream():
+    """A batch of few distinct tokens, repeated, with some outside the
+    vocabulary (which gather no embedding row and get no gradient): the
+    two-stream step equals the one-stream step bit for bit over two steps,
+    disagreements included."""
+    cfg = S.GPT_TEST4
+    rng = np.random.default_rng(77)
+    tokens = rng.integers(0, 12, (cfg.batch, cfg.seq + 1)).astype(np.int32)
+    tokens[0, ::7] = -1
+    tokens[1, 3::11] = cfg.vocab + 5
+    outs = []
+    for two in (True, False):
+        params, _, peers, m = gpt_setup(cfg, two)
+        td = torch.from_numpy(tokens).to(DEV)
+        dis = torch.zeros(m.n_units, dtype=torch.float32, device=DEV)
+        torch.cuda.synchronize()
+        for s in range(2):
+            hp, _ = gpt_hp(cfg, s + 1)
+            LU.layup_step(m.ctx, td, None, hp, cfg.alpha, 0, None, dis)
+        m.synchronize()
+        outs.append([t.clone() for t in (m.params, m.m, m.v, m.grads, m.params_bf16)] + [dis.clone()])
+        assert m.read_trace() == [(s, u) for s in range(2) for u in range(m.n_units - 1, -1, -1)]
+        m.close()
+        del m
+    for name, a, b in zip(("params", "m", "v", "grads", "bf16 copy", "disagreement"), outs[0], outs[1]):
+        assert torch.equal(a, b), name
+
+
 def test_gpt_manual_unit_calls_match_step():
     """Driving forward / backward(u) / update(u) by hand equals layup_step, and
     out-of-order calls are refused."""
