@@ -201,8 +201,7 @@ struct layup_ctx {
   // ev_mid[p]: the first half of block parity p's operands written (dfb, dyB;
   // compute stream) -- the others (dyA, dqb) are covered by the unit events;
   // ev_rd[k][p]: operand k's dW GEMM and bias sum done (update stream);
-  // ev_dx: a dX GEMM issued (fused schedule: dW runs after it)
-  hipEvent_t ev_mid[2] = {}, ev_rd[4][2] = {}, ev_dx = nullptr;
+  hipEvent_t ev_mid[2] = {}, ev_rd[4][2] = {};
   hipEvent_t ev_head = nullptr;  // the head's dW done (update stream)
   hipEvent_t ev_sort = nullptr;  // the token sort done (update stream)
   hipEvent_t ev_fwd_half = nullptr;  // the forward's second half done (update stream)
@@ -553,16 +552,17 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   bf16_t *dyA = c->dyA[pq], *df16 = c->dfb[pq], *dyB = c->dyB[pq], *dq16 = c->dqb[pq];
   // Every linear layer: dX on the compute stream (the critical path), then
   // dW and db.  In the fused schedule the dW GEMM updates the weight in
-  // place, so it waits for the layer's dX (which reads the weight first).
+  // place, so it must follow the layer's dX (which reads the weight first):
+  // the MLP output projection's dW is issued after the event that follows
+  // the MLP's dX GEMMs (ev_mid) and the attention projection's after the
+  // unit event, the same events the other dW GEMMs wait for (an extra event
+  // record per layer on the compute stream costs it a few microseconds of
+  // idle time each).
   const bool fz = c->fused_dw;
   // The bias gradient (column sums of dY) comes out of the same dW GEMM: its
   // A operand is dY^T, whose row sums it accumulates from the fragments.
   auto weight_grads = [&](int op, Gemm dw, const std::string& wname, const char* bname,
                           const char* what) -> layup_status {
-    if (fz) {
-      HIPCHK(c, rec(c->ev_dx, s), "record dX issued");
-      HIPCHK(c, wait(sw, c->ev_dx), "wait dX");
-    }
     dw.rowsum = fl.g(p + bname);
     TRY(run_gemm(c, dw_gemm(c, dw, wname), sw, what, true));
     HIPCHK(c, rec(c->ev_rd[op][pq], sw), "record operand read");
@@ -575,8 +575,8 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   TRY(run_gemm(c, dg, s, "mproj dX + gelu backward", true));
   // dyA was written before the previous unit event, which the update stream
   // has waited for
-  TRY(weight_grads(OP_A, mk(false, false, d, F, N, dyA, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32),
-                   p + "mproj.w", "mproj.b", "mproj dW + db"));
+  const Gemm mproj_dw = mk(false, false, d, F, N, dyA, d, A.gl, F, fl.g(p + "mproj.w"), F, EPI_F32);
+  if (!fz) TRY(weight_grads(OP_A, mproj_dw, p + "mproj.w", "mproj.b", "mproj dW + db"));
   // MLP input projection: dY = df16
   Gemm fcx = mk(true, false, N, d, F, df16, F, fl.w16(p + "fc.w"), d, c->da, d, EPI_F32);
   TRY(run_gemm(c, fcx, s, "fc dX", true));
@@ -588,13 +588,14 @@ layup_status gpt_backward(layup_ctx* c, int u) {
   // costs a few microseconds of idle time there)
   HIPCHK(c, rec(c->ev_mid[pq], s), "record operands written");
   HIPCHK(c, wait(sw, c->ev_mid[pq]), "wait operands written");
+  if (fz) TRY(weight_grads(OP_A, mproj_dw, p + "mproj.w", "mproj.b", "mproj dW + db"));
   TRY(weight_grads(OP_F, mk(false, false, F, d, N, df16, F, A.a2, d, fl.g(p + "fc.w"), d, EPI_F32),
                    p + "fc.w", "fc.b", "fc dW + db"));
   // attention output projection: dY = dyB = bf16(dh) from the LayerNorm backward above
   Gemm prx = mk(true, false, N, d, d, dyB, d, fl.w16(p + "proj.w"), d, c->do16, d, EPI_BF16);
   TRY(run_gemm(c, prx, s, "proj dX", true));
-  TRY(weight_grads(OP_B, mk(false, false, d, d, N, dyB, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32),
-                   p + "proj.w", "proj.b", "proj dW + db"));
+  const Gemm proj_dw = mk(false, false, d, d, N, dyB, d, A.o, d, fl.g(p + "proj.w"), d, EPI_F32);
+  if (!fz) TRY(weight_grads(OP_B, proj_dw, p + "proj.w", "proj.b", "proj dW + db"));
   HIPCHK(c, wait(s, c->ev_rd[OP_Q][pq]), "wait operand free");
   if (A.of) {
     // attention core, fused: dQ, dK, dV from recomputed scores (P and dS stay
@@ -649,6 +650,7 @@ layup_status gpt_backward(layup_ctx* c, int u) {
     HIPCHK(c, hipStreamWaitEvent(sw, c->ev_unit[u], 0), "wait unit event");
     c->unit_recorded = true;
   }
+  if (fz) TRY(weight_grads(OP_B, proj_dw, p + "proj.w", "proj.b", "proj dW + db"));
   TRY(weight_grads(OP_Q, mk(false, false, 3 * d, d, N, dq16, 3 * d, A.a, d, fl.g(p + "qkv.w"), d, EPI_F32),
                    p + "qkv.w", "qkv.b", "qkv dW + db"));
   if (side && l == (int)g.n_layer - 1) {
@@ -1002,8 +1004,7 @@ layup_status layup_init(layup_ctx** out, const layup_config* cfg, const layup_bu
     return fail(nullptr, LAYUP_ERR_HIP, "event creation failed");
   }
   // ordering events between the compute stream and the update stream's dW work
-  bool ev_ok = hipEventCreateWithFlags(&c->ev_dx, hipEventDisableTiming) == hipSuccess;
-  ev_ok = ev_ok && hipEventCreateWithFlags(&c->ev_head, hipEventDisableTiming) == hipSuccess &&
+  bool ev_ok = hipEventCreateWithFlags(&c->ev_head, hipEventDisableTiming) == hipSuccess &&
           hipEventCreateWithFlags(&c->ev_sort, hipEventDisableTiming) == hipSuccess &&
           hipEventCreateWithFlags(&c->ev_fwd_half, hipEventDisableTiming) == hipSuccess;
   for (int q = 0; q < 2; ++q) {
@@ -1034,7 +1035,6 @@ void layup_destroy(layup_ctx* ctx) {
   for (auto& row : ctx->ev_rd)
     for (auto e : row)
       if (e) hipEventDestroy(e);
-  if (ctx->ev_dx) hipEventDestroy(ctx->ev_dx);
   if (ctx->ev_head) hipEventDestroy(ctx->ev_head);
   if (ctx->ev_sort) hipEventDestroy(ctx->ev_sort);
   if (ctx->ev_fwd_half) hipEventDestroy(ctx->ev_fwd_half);
