@@ -195,8 +195,12 @@ layup_status layup_refresh_shadow(layup_ctx* ctx);
  *   MLP: tokens device int32 [batch] class labels; x device float32
  *        [batch, mlp_dims[0]].
  * loss_out: device float32 scalar (nullable).  Enqueued on the compute
- * stream.  Valid only once the previous step's updates are done (the library
- * orders this itself through the streams). */
+ * stream (with a separate update stream, half of the batch and the token
+ * sort on that stream).  Valid only once the previous step's updates are
+ * done (the library orders this itself through the streams).  tokens and x
+ * are read asynchronously: the caller keeps them allocated and unchanged
+ * until the step's work on both streams is done (the compute stream's join
+ * at the end of layup_step_ex, or layup_synchronize). */
 layup_status layup_forward(layup_ctx* ctx, const int32_t* tokens, const float* x, float* loss_out);
 
 /* Backward pass of one unit (Algorithm 1 "Backward pass at layer l"):

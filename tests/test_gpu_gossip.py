@@ -189,7 +189,8 @@ def test_gossip_gpt_replicas_match_oracle():
         t[i] += 1
         hp = LU.hparams("adamw", cfg.lr, 0.0, cfg.weight_decay, cfg.beta1, cfg.beta2, cfg.eps, t[i])
         alpha = LU.layup_push_sum_send(w, i, j)
-        LU.layup_step_ex(models[i].ctx, _dev(tokens), None, hp, alpha, mix_mode=LU.LAYUP_MIX_PUSH,
+        td = _dev(tokens)     # read asynchronously by the step: kept until it is done
+        LU.layup_step_ex(models[i].ctx, td, None, hp, alpha, mix_mode=LU.LAYUP_MIX_PUSH,
                          push_params=models[j].params, push_params_bf16=models[j].params_bf16,
                          loss_out=loss)
         LU.layup_push_sum_receive(w, i, j)
