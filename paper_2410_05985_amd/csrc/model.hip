@@ -401,15 +401,22 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
                 dh = d / H, Vp = align64(g.vocab);
   const float scale = 1.0f / sqrtf((float)dh);
   Flat fl{c};
-  // The forward of sequences [b0, b0 + nb) on stream st.  With an update
+  // The forward of sequences [b0, b0 + nb) on stream st, in three pieces
+  // (embedding, block l, final LayerNorm + head + loss).  With an update
   // stream (idle during the forward) the batch is taken in two halves, the
-  // second there; every row's arithmetic is the same either way.
-  auto part = [&](int64_t b0, int64_t nb, hipStream_t st) -> layup_status {
-    const int64_t r0 = b0 * T, n = nb * T;
+  // second there, and the two halves' pieces are enqueued alternately so
+  // that both streams have work from the start; every row's arithmetic is
+  // the same either way.
+  auto embed = [&](int64_t b0, int64_t nb, hipStream_t st) -> layup_status {
+    const int64_t r0 = b0 * T;
     const int32_t* tk = tokens + b0 * (T + 1);
     HIPCHK(c, launch_embed_fwd(tk, fl.p("wte"), fl.p("wpe"), c->acts[0].x + r0 * d, (int)nb, (int)T, (int)d,
                                g.vocab, st), "embedding");
-    for (int l = 0; l < g.n_layer; ++l) {
+    return LAYUP_OK;
+  };
+  auto block = [&](int l, int64_t b0, int64_t nb, hipStream_t st) -> layup_status {
+    const int64_t r0 = b0 * T, n = nb * T;
+    {
       BlockActs& A = c->acts[l];
       const std::string p = "h" + std::to_string(l) + ".";
       float* x_next = ((l + 1 < g.n_layer) ? c->acts[l + 1].x : c->xL) + r0 * d;
@@ -465,6 +472,11 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
       mp.aux = A.h + r0 * d;
       TRY(run_gemm(c, mp, st, "mproj forward"));
     }
+    return LAYUP_OK;
+  };
+  auto tail = [&](int64_t b0, int64_t nb, hipStream_t st) -> layup_status {
+    const int64_t r0 = b0 * T, n = nb * T;
+    const int32_t* tk = tokens + b0 * (T + 1);
     HIPCHK(c, launch_layernorm_fwd(c->xL + r0 * d, fl.p("lnf.g"), fl.p("lnf.b"), c->xf + r0 * d, c->meanf + r0,
                                    c->rstdf + r0, n, (int)d, st), "lnf");
     Gemm hd = mk(true, true, n, Vp, d, c->xf + r0 * d, d, fl.w16("wte"), d, c->logits + r0 * Vp, Vp, EPI_BF16);
@@ -480,8 +492,15 @@ layup_status gpt_forward(layup_ctx* c, const int32_t* tokens, float* loss_out) {
   if (side) HIPCHK(c, hipStreamWaitEvent(s2, c->ev_start, 0), "wait step start");
   // one stream: the whole batch at once (half-size products are less efficient)
   const int64_t nb0 = (side && B >= 2) ? B / 2 : B;
-  TRY(part(0, nb0, s));
-  if (nb0 < B) TRY(part(nb0, B - nb0, s2));
+  const bool two = nb0 < B;
+  TRY(embed(0, nb0, s));
+  if (two) TRY(embed(nb0, B - nb0, s2));
+  for (int l = 0; l < g.n_layer; ++l) {
+    TRY(block(l, 0, nb0, s));
+    if (two) TRY(block(l, nb0, B - nb0, s2));
+  }
+  TRY(tail(0, nb0, s));
+  if (two) TRY(tail(nb0, B - nb0, s2));
   if (side) {
     HIPCHK(c, hipEventRecord(c->ev_fwd_half, s2), "record forward half");
     HIPCHK(c, hipStreamWaitEvent(s, c->ev_fwd_half, 0), "wait forward half");
