@@ -126,6 +126,14 @@ GPT2_SMALL_2L = GPTConfig(n_layer=2, d_model=768, n_head=12, d_ff=3072, seq=1024
 GPT_TEST_T2048 = GPTConfig(n_layer=1, d_model=256, n_head=2, d_ff=512, seq=2048, batch=1, vocab=300,
                            name="gpt-test-t2048-dh128")
 
+# The GPT-2-medium and 1.3B stacks' widths (1024 features, 16 heads of 64,
+# MLP 4096; 2048 features, 16 heads of 128, MLP 8192) with one block and a
+# short sequence: their LayerNorm row widths, head widths and GEMM shapes.
+GPT_TEST_W1024 = GPTConfig(n_layer=1, d_model=1024, n_head=16, d_ff=4096, seq=256, batch=2, vocab=2000,
+                           name="gpt-test-medium-width")
+GPT_TEST_W2048 = GPTConfig(n_layer=1, d_model=2048, n_head=16, d_ff=8192, seq=128, batch=2, vocab=500,
+                           name="gpt-test-1.3b-width")
+
 RESNET50_UPDATE = dict(lr=0.1, momentum=0.9, weight_decay=5e-5, alpha=0.5)
 
 # ------------------------------------------------------------ param specs

@@ -152,6 +152,7 @@ def test_gpt_forward_activations(cfg):
 
 @pytest.mark.parametrize("cfg", [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48,
                                  S.GPT_TEST_W832, S.GPT_TEST_W1088, S.GPT_TEST4, S.GPT2_SMALL_2L,
+                                 S.GPT_TEST_W1024, S.GPT_TEST_W2048,
                                  S.GPT_TEST_T2048],
                          ids=lambda c: c.name)
 def test_gpt_step_parity(cfg):

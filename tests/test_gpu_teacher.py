@@ -28,7 +28,8 @@ GRAD_RTOL = 2e-2
 UPDATE_RTOL = 1e-5
 
 TEACHER_CASES = [S.GPT_TEST, S.GPT_TEST_RAGGED, S.GPT_TEST_DH128, S.GPT_TEST_DH48, S.GPT_TEST_W832,
-                 S.GPT_TEST_LONG, S.GPT_TEST4, S.GPT2_SMALL_2L, S.GPT_TEST_T2048]
+                 S.GPT_TEST_LONG, S.GPT_TEST4, S.GPT2_SMALL_2L, S.GPT_TEST_T2048, S.GPT_TEST_W1024,
+                 S.GPT_TEST_W2048]
 
 
 @pytest.mark.parametrize("cfg", TEACHER_CASES, ids=lambda c: c.name)
